@@ -1,0 +1,248 @@
+/*
+ * mw.h - C ABI of the MI355X (gfx950) paged grouped-query attention library
+ * for prefill/decode multiplexing on split compute units.
+ *
+ * The paper's statement of the problem: prefill and decode run at the same
+ * time on disjoint sets of compute units of one GPU (Sec. 2.4 and Sec. 3.2.1),
+ * both phases read and extend one paged KV-cache pool kept in the GPU's shared
+ * memory space (Sec. 2.4; PagedAttention in Related Work), and each launch's
+ * latency feeds the scheduler's estimates (Sec. 3.3).  AMD GPUs give the
+ * intra-process partition through CU-masked streams (Sec. 5, Discussion).
+ * This header exposes exactly those pieces:
+ *
+ *   mw_kv_pool_*   paged K/V pool descriptor, host page allocator, KV append
+ *   mw_partition_* two CU-masked HIP streams with disjoint compute units
+ *   mw_prefill_attn causal prefill attention of new tokens over a cached prefix
+ *   mw_decode_attn  decode attention, one query token per sequence
+ *   mw_timing_*    per-call GPU timings (HIP events)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Status: every call returns mw_status (0 = MW_OK, negative = error) and
+ *   never throws across the ABI.  The text of the last error of the calling
+ *   thread is returned by mw_last_error().
+ * - Ownership: every device buffer (pools, block tables, Q, O, workspaces) is
+ *   owned by the caller; the library never frees one.  Handles (pool
+ *   metadata, partitions and their streams, timing events) are owned by the
+ *   library and released by the matching *_destroy call.
+ * - Streams: an mw_stream is a hipStream_t; NULL means the null stream of
+ *   the current device.
+ * - Asynchrony: attention and pool-write calls only enqueue work.  They do
+ *   no host<->device copies (a copy would serialise the two partitions), so
+ *   lengths are passed twice: a host copy for planning and validation and a
+ *   device copy for the kernels.  The two copies must hold the same values.
+ * - Data types: K, V, Q and O are bf16 (raw 16-bit patterns); scores,
+ *   softmax and accumulation are fp32.  Only head_dim 128 and page size 16
+ *   are supported (MW_ERR_UNSUPPORTED otherwise).
+ * - Layouts:
+ *     K and V pools : [num_pages][num_kv_heads][page_size][head_dim] bf16,
+ *                     so one (page, kv head) block is 4 KiB contiguous.
+ *     block tables  : int32 [rows][bt_stride], row-major; entry t/page_size
+ *                     of a row is the page holding token t of that sequence
+ *                     (slot t % page_size).
+ *     Q and O       : [tokens][num_q_heads][head_dim] bf16.
+ *   Query head h reads KV head h / (num_q_heads / num_kv_heads).
+ * - Device-side page indices outside [0, num_pages) are never dereferenced:
+ *   kernels treat such a page as zeros (results are then meaningless, but no
+ *   memory outside the pool is touched).
+ * - Asynchronous HIP faults surface as MW_ERR_HIP from the next call that
+ *   synchronises (mw_timing_elapsed, mw_sync), with the HIP error text in
+ *   mw_last_error().
+ */
+#ifndef MW_H
+#define MW_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t mw_status;
+#define MW_OK 0
+#define MW_ERR_INVALID_ARG (-1)  /* a bad argument; nothing was enqueued        */
+#define MW_ERR_UNSUPPORTED (-2)  /* valid but not implemented (head_dim, page)  */
+#define MW_ERR_OUT_OF_PAGES (-3) /* the host page allocator has too few pages   */
+#define MW_ERR_HIP (-4)          /* the HIP runtime reported an error           */
+#define MW_ERR_NOT_READY (-5)    /* a timing was read before it was recorded    */
+
+typedef void *mw_stream; /* a hipStream_t */
+
+/* Text of the calling thread's last error ("" if none).  The pointer stays
+ * valid until the thread's next failing call. */
+const char *mw_last_error(void);
+
+/* Library ABI version (increments on any signature change). */
+int32_t mw_version(void);
+
+/* Waits for all work on `stream` and reports any pending HIP error. */
+mw_status mw_sync(mw_stream stream);
+
+/* ------------------------------------------------------------------------
+ * KV pool (Sec. 2.4: one KV-cache pool shared by both phases; paged as in
+ * PagedAttention).  The device arrays belong to the caller; the handle holds
+ * their addresses, the geometry, and a host free-list of page ids.
+ * ---------------------------------------------------------------------- */
+typedef struct mw_kv_pool mw_kv_pool;
+typedef struct {
+    int32_t num_pages;    /* pages in each of the K and V arrays (>= 1)      */
+    int32_t page_size;    /* tokens per page; must be 16                     */
+    int32_t num_kv_heads; /* >= 1                                            */
+    int32_t head_dim;     /* must be 128                                     */
+} mw_kv_pool_desc;
+
+/* Registers caller-owned device arrays d_k_pages / d_v_pages, each
+ * num_pages*num_kv_heads*page_size*head_dim bf16 elements, 16-byte aligned.
+ * The free list starts as 0, 1, ..., num_pages-1. */
+mw_status mw_kv_pool_create(const mw_kv_pool_desc *desc, void *d_k_pages, void *d_v_pages,
+                            mw_kv_pool **out);
+mw_status mw_kv_pool_destroy(mw_kv_pool *pool);
+/* Replaces the free list by `perm` (n distinct page ids in [0, num_pages)),
+ * popped front first.  Lets a caller deal pages in a random order. */
+mw_status mw_kv_pool_set_free_order(mw_kv_pool *pool, const int32_t *perm, int32_t n);
+/* Pops n_pages ids from the free list into host array pages_out.  Fails with
+ * MW_ERR_OUT_OF_PAGES (taking nothing) if fewer are free. */
+mw_status mw_kv_pool_alloc(mw_kv_pool *pool, int32_t n_pages, int32_t *pages_out);
+/* Returns pages to the back of the free list.  A page already free, or out
+ * of range, is MW_ERR_INVALID_ARG (and nothing is returned). */
+mw_status mw_kv_pool_free(mw_kv_pool *pool, const int32_t *pages, int32_t n_pages);
+mw_status mw_kv_pool_num_free(const mw_kv_pool *pool, int32_t *n_free);
+
+/* KV append (Sec. 2.1: each step stores the new tokens' keys and values in
+ * the cache).  For each sequence b < batch, copies the rows
+ * d_k_new[d_qo_indptr[b] + i] and d_v_new[...] (each [num_kv_heads][head_dim]
+ * bf16) for i < h_new_lens[b] into position d_start_pos[b] + i of the
+ * sequence whose block-table row is b.  A pure bit copy.
+ *   h_new_lens  host  [batch]   new tokens per sequence (>= 0)
+ *   h_start_pos host  [batch]   first position written (>= 0); validated
+ *                               against bt_stride*page_size
+ *   d_qo_indptr device[batch+1] row offsets into d_k_new / d_v_new
+ *   d_start_pos device[batch]   same values as h_start_pos
+ *   d_block_table device [batch][bt_stride]
+ * `timing` may be NULL. */
+typedef struct mw_timing mw_timing;
+mw_status mw_kv_pool_write(const mw_kv_pool *pool, int32_t batch, const int32_t *h_new_lens,
+                           const int32_t *h_start_pos, const int32_t *d_qo_indptr,
+                           const int32_t *d_start_pos, const int32_t *d_block_table,
+                           int32_t bt_stride, const void *d_k_new, const void *d_v_new,
+                           mw_stream stream, mw_timing *timing);
+
+/* Gathers tokens [0, n_tokens) of one sequence (block-table row
+ * d_block_table[0 .. ceil(n_tokens/page_size))) into contiguous
+ * [n_tokens][num_kv_heads][head_dim] arrays.  A bit copy used by tests to
+ * check the paging arithmetic the attention kernels share. */
+mw_status mw_kv_pool_gather(const mw_kv_pool *pool, const int32_t *d_block_table,
+                            int32_t n_tokens, void *d_k_out, void *d_v_out, mw_stream stream);
+
+/* ------------------------------------------------------------------------
+ * CU partition (Sec. 3.2.1: bind each phase's stream to its own compute
+ * units; Sec. 5: hipExtStreamCreateWithCUMask on AMD GPUs).
+ * MI355X has 8 XCDs of 32 CUs and dispatches workgroups round-robin over the
+ * XCDs, so each partition takes the same number of CUs on every XCD: CU
+ * counts must be multiples of 8, at least 8 each, and sum to at most the
+ * device's CU count.  The masks are 32-bit words, bit i of word w naming
+ * CU (32*w + i) in the runtime's CU numbering.
+ * ---------------------------------------------------------------------- */
+typedef struct mw_partition mw_partition;
+/* Creates two streams on `device`: prefill on prefill_cus CUs and decode on
+ * decode_cus disjoint CUs. */
+mw_status mw_partition_create(int32_t device, int32_t prefill_cus, int32_t decode_cus,
+                              mw_partition **out);
+/* Same, from explicit masks of n_words 32-bit words each (must be disjoint
+ * and non-empty). */
+mw_status mw_partition_create_masks(int32_t device, const uint32_t *prefill_mask,
+                                    const uint32_t *decode_mask, int32_t n_words,
+                                    mw_partition **out);
+mw_status mw_partition_streams(const mw_partition *part, mw_stream *prefill,
+                               mw_stream *decode);
+/* Copies the masks out (n_words = 8 words each, unused words zero). */
+mw_status mw_partition_masks(const mw_partition *part, uint32_t *prefill_mask,
+                             uint32_t *decode_mask);
+/* Synchronises both streams, then destroys them. */
+mw_status mw_partition_destroy(mw_partition *part);
+
+/* Launches n_blocks one-wave workgroups on `stream` that each record the
+ * hardware ids of the CU they run on and a start/end timestamp:
+ * d_out[4*b + 0] = XCC id, [+1] = HW_ID register (CU, SIMD, shader array,
+ * shader engine fields), [+2] = start and [+3] = end of a spin of spin_cycles
+ * shader clocks (low 32 bits of the 100 MHz real-time counter). */
+mw_status mw_cu_probe(int32_t n_blocks, int32_t spin_cycles, uint32_t *d_out,
+                      mw_stream stream);
+
+/* ------------------------------------------------------------------------
+ * Per-call timing.  A call given a timing handle records a start event, one
+ * event after each kernel it launches, and (implicitly) a stop event = the
+ * last one, all on its stream.
+ * ---------------------------------------------------------------------- */
+mw_status mw_timing_create(mw_timing **out);
+mw_status mw_timing_destroy(mw_timing *t);
+/* Records only a start event on `stream` (a reference point for offsets). */
+mw_status mw_timing_mark(mw_timing *t, mw_stream stream);
+/* Waits for the stop event.  gpu_ms = stop - start; host_launch_ms = host
+ * wall time the recording call spent enqueueing.  Either output may be NULL. */
+mw_status mw_timing_elapsed(mw_timing *t, float *gpu_ms, float *host_launch_ms);
+/* Number of kernels recorded and the GPU time of kernel k (event k to k+1). */
+mw_status mw_timing_kernels(mw_timing *t, int32_t *n_kernels);
+mw_status mw_timing_kernel_ms(mw_timing *t, int32_t k, float *ms);
+/* Start and stop of t relative to ref's start event, in ms. */
+mw_status mw_timing_offsets(mw_timing *t, mw_timing *ref, float *start_ms, float *stop_ms);
+
+/* ------------------------------------------------------------------------
+ * Attention.  For output row i of a sequence with nvis visible keys and query
+ * head h (kv = h / (Hq/Hkv)):
+ *     O[i][h] = softmax_j(scale * Q[i][h] . K[j][kv]) V[j][kv],  j < nvis
+ * Prefill with a cached prefix (Sec. 3.3, Table "tab:theory_cost": n new
+ * tokens against L = r + n keys; Sec. 1: a chunk reads the KV of every
+ * earlier chunk): row i of a sequence with prefix r sees keys 0 .. r+i
+ * (nvis = r + i + 1).  Decode (same table: r + 1 keys): the sequence's own
+ * new K/V is already in the pool at position L-1, and its query sees keys
+ * 0 .. L-1 (nvis = L).  Every K/V row is read through the block table.
+ * ---------------------------------------------------------------------- */
+typedef struct {
+    int32_t num_q_heads;  /* multiple of num_kv_heads                      */
+    int32_t num_kv_heads; /* must equal the pool's                         */
+    int32_t head_dim;     /* must be 128                                   */
+    float scale;          /* softmax scale, usually 1/sqrt(head_dim)       */
+} mw_attn_shape;
+
+/* Causal prefill for `batch` sequences (varlen).
+ *   h_new_lens, h_prefix_lens host [batch]: n_b >= 0, r_b >= 0, with
+ *       r_b + n_b <= bt_stride * page_size
+ *   d_qo_indptr   device [batch+1]: rows of sequence b are
+ *       [d_qo_indptr[b], d_qo_indptr[b+1]) of d_q / d_out
+ *   d_prefix_lens device [batch]
+ *   d_block_table device [batch][bt_stride]; must map every position
+ *       < r_b + n_b (the new tokens' K/V are written before this call)
+ *   d_q, d_out    device [sum n][num_q_heads][head_dim] bf16, 16-B aligned
+ * One kernel launch; `timing` may be NULL. */
+mw_status mw_prefill_attn(const mw_kv_pool *pool, const mw_attn_shape *shape, int32_t batch,
+                          const int32_t *h_new_lens, const int32_t *h_prefix_lens,
+                          const int32_t *d_qo_indptr, const int32_t *d_prefix_lens,
+                          const int32_t *d_block_table, int32_t bt_stride, const void *d_q,
+                          void *d_out, mw_stream stream, mw_timing *timing);
+
+/* Decode is split over chunks of `chunk_pages` pages of each sequence
+ * (0 = default 16) and merged by a second kernel (log-sum-exp combine).  The
+ * split depends only on the lengths, never on page ids.
+ * Workspace bytes for a call with these lengths: */
+mw_status mw_decode_workspace_size(const mw_attn_shape *shape, int32_t batch,
+                                   const int32_t *h_seq_lens, int32_t chunk_pages,
+                                   size_t *bytes);
+/*   h_seq_lens host [batch], d_seq_lens device [batch]: L_b >= 1,
+ *       L_b <= bt_stride * page_size
+ *   d_block_table device [batch][bt_stride]
+ *   d_q, d_out device [batch][num_q_heads][head_dim] bf16
+ *   d_workspace device, >= mw_decode_workspace_size bytes, 16-B aligned
+ * Two kernel launches (split, combine); `timing` may be NULL. */
+mw_status mw_decode_attn(const mw_kv_pool *pool, const mw_attn_shape *shape, int32_t batch,
+                         const int32_t *h_seq_lens, const int32_t *d_seq_lens,
+                         const int32_t *d_block_table, int32_t bt_stride, const void *d_q,
+                         void *d_out, void *d_workspace, size_t workspace_bytes,
+                         int32_t chunk_pages, mw_stream stream, mw_timing *timing);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MW_H */

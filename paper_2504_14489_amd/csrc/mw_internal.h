@@ -1,0 +1,68 @@
+// Internal declarations shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <chrono>
+#include <cstdint>
+#include <deque>
+#include <vector>
+
+#include "mw.h"
+
+namespace mw {
+
+constexpr int kHeadDim = 128;
+constexpr int kPageSize = 16;
+constexpr int kMaxTimingEvents = 8;
+
+// Records `msg` as the calling thread's last error and returns `st`.
+mw_status fail(mw_status st, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+
+inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+}  // namespace mw
+
+#define MW_HIP_TRY(expr)                                                                  \
+    do {                                                                                  \
+        hipError_t mw_e_ = (expr);                                                        \
+        if (mw_e_ != hipSuccess)                                                          \
+            return mw::fail(MW_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(mw_e_)); \
+    } while (0)
+
+struct mw_kv_pool {
+    mw_kv_pool_desc desc;
+    uint16_t *k;
+    uint16_t *v;
+    std::deque<int32_t> free_list;
+    std::vector<uint8_t> is_free;
+};
+
+struct mw_timing {
+    hipEvent_t ev[mw::kMaxTimingEvents];
+    int n_events;          // events recorded by the last call (start + one per kernel)
+    bool created;
+    double host_ms;        // host time spent enqueueing
+    std::chrono::steady_clock::time_point t0;
+};
+
+struct mw_partition {
+    int device;
+    hipStream_t prefill;
+    hipStream_t decode;
+    uint32_t prefill_mask[8];
+    uint32_t decode_mask[8];
+};
+
+namespace mw {
+
+// Timing helpers: begin() records the start event, kernel_done() one event per
+// kernel, end() the host-side duration.  All are no-ops for a NULL handle.
+mw_status timing_begin(mw_timing *t, hipStream_t s);
+mw_status timing_kernel_done(mw_timing *t, hipStream_t s);
+void timing_end(mw_timing *t);
+
+// Reports a failed kernel launch (bad configuration) as MW_ERR_HIP.
+mw_status check_launch(const char *what);
+
+}  // namespace mw

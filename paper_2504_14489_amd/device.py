@@ -1,0 +1,169 @@
+"""A synthetic workload resident in GPU memory, driven through the C ABI.
+
+Glue used by the tests, the benchmark and the smoke check: torch allocates
+the device buffers (pools, block tables, Q, O, workspaces) and every step of
+the attention path runs in the library's HIP kernels via :mod:`.mw`.
+"""
+from __future__ import annotations
+
+import math
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+import torch
+
+from . import mw
+from .workloads import Workload
+
+
+def _dev16(a: np.ndarray, device) -> torch.Tensor:
+    """uint16 numpy -> int16 device tensor with the same bits."""
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(device)
+
+
+def _dev32(a, device) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(np.asarray(a, dtype=np.int32))).to(device)
+
+
+def to_bits(t: torch.Tensor) -> np.ndarray:
+    """Device bf16/int16 tensor -> uint16 numpy bits."""
+    if t.dtype == torch.bfloat16:
+        t = t.view(torch.int16)
+    return t.cpu().numpy().view(np.uint16)
+
+
+def bits_to_f32(b: np.ndarray) -> np.ndarray:
+    return (np.asarray(b, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+class DeviceWorkload:
+    """Uploads a :class:`Workload` and registers its pool with the library."""
+
+    def __init__(self, wl: Workload, device: str = "cuda:0", copies: int = 1):
+        self.wl = wl
+        self.cfg = wl.cfg
+        self.device = torch.device(device)
+        c = wl.cfg
+        self.hq, self.hkv, self.d = c.hq, c.hkv, c.head_dim
+        self.scale = 1.0 / math.sqrt(c.head_dim)
+        self.k_pool = _dev16(wl.k_pool, self.device)
+        self.v_pool = _dev16(wl.v_pool, self.device)
+        self.pool = mw.mw_kv_pool_create(wl.num_pages, c.page_size, c.hkv, c.head_dim,
+                                         self.k_pool.data_ptr(), self.v_pool.data_ptr())
+        self.pre_bt = _dev32(wl.pre_bt[None, :], self.device)
+        self.dec_bt = _dev32(wl.dec_bt, self.device)
+        self.dec_lens = wl.dec_lens.astype(np.int32)
+        self.d_dec_lens = _dev32(self.dec_lens, self.device)
+        self.q_pre = _dev16(wl.q_pre, self.device)
+        self.q_dec = _dev16(wl.q_dec, self.device)
+        self.o_pre = torch.zeros_like(self.q_pre)
+        self.o_dec = torch.zeros_like(self.q_dec)
+        self._ws = {}
+        self._pre_args = {}
+        self._dec_start = None
+
+    def close(self):
+        if self.pool is not None:
+            mw.mw_kv_pool_destroy(self.pool)
+            self.pool = None
+
+    # ----------------------------------------------------------- prefill --
+    def _prefill_args(self, r: int, n: int):
+        key = (r, n)
+        if key not in self._pre_args:
+            self._pre_args[key] = (_dev32([0, n], self.device), _dev32([r], self.device))
+        return self._pre_args[key]
+
+    def prefill(self, r: int, n: int, stream=0, timing=None, out: Optional[torch.Tensor] = None):
+        """Causal prefill of positions [r, r+n) over prefix r; returns the
+        output rows [n][Hq][D] (a view of ``out`` or of the workload's buffer)."""
+        indptr, pref = self._prefill_args(r, n)
+        q = self.q_pre[r:r + n]
+        o = self.o_pre[r:r + n] if out is None else out
+        mw.mw_prefill_attn(self.pool, self.hq, self.hkv, self.d, self.scale, [n], [r],
+                           indptr.data_ptr(), pref.data_ptr(), self.pre_bt.data_ptr(),
+                           self.pre_bt.shape[1], q.data_ptr(), o.data_ptr(), stream, timing)
+        return o
+
+    def write_prefill_kv(self, r: int, n: int, k_new: torch.Tensor, v_new: torch.Tensor,
+                         stream=0, timing=None):
+        indptr, pref = self._prefill_args(r, n)
+        mw.mw_kv_pool_write(self.pool, [n], [r], indptr.data_ptr(), pref.data_ptr(),
+                            self.pre_bt.data_ptr(), self.pre_bt.shape[1], k_new.data_ptr(),
+                            v_new.data_ptr(), stream, timing)
+
+    # ------------------------------------------------------------ decode --
+    def workspace(self, chunk_pages: int = 0) -> torch.Tensor:
+        if chunk_pages not in self._ws:
+            nbytes = mw.mw_decode_workspace_size(self.hq, self.hkv, self.d, self.dec_lens,
+                                                 chunk_pages)
+            self._ws[chunk_pages] = torch.empty(max(nbytes, 16), dtype=torch.uint8,
+                                                device=self.device)
+        return self._ws[chunk_pages]
+
+    def decode(self, stream=0, timing=None, chunk_pages: int = 0,
+               out: Optional[torch.Tensor] = None):
+        ws = self.workspace(chunk_pages)
+        o = self.o_dec if out is None else out
+        mw.mw_decode_attn(self.pool, self.hq, self.hkv, self.d, self.scale, self.dec_lens,
+                          self.d_dec_lens.data_ptr(), self.dec_bt.data_ptr(), self.dec_bt.shape[1],
+                          self.q_dec.data_ptr(), o.data_ptr(), ws.data_ptr(), ws.numel(),
+                          chunk_pages, stream, timing)
+        return o
+
+    def write_decode_kv(self, k_new: torch.Tensor, v_new: torch.Tensor, stream=0, timing=None):
+        """Appends each decode sequence's newest token at position L-1."""
+        B = len(self.dec_lens)
+        if self._dec_start is None:
+            self._dec_start = (_dev32(np.arange(B + 1), self.device),
+                               _dev32(self.dec_lens - 1, self.device))
+        indptr, start = self._dec_start
+        mw.mw_kv_pool_write(self.pool, np.ones(B, np.int32), self.dec_lens - 1,
+                            indptr.data_ptr(), start.data_ptr(), self.dec_bt.data_ptr(),
+                            self.dec_bt.shape[1], k_new.data_ptr(), v_new.data_ptr(), stream,
+                            timing)
+
+
+class Timing:
+    """Owns an mw_timing handle."""
+
+    def __init__(self):
+        self.h = mw.mw_timing_create()
+
+    def close(self):
+        if self.h is not None:
+            mw.mw_timing_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def elapsed(self) -> Tuple[float, float]:
+        return mw.mw_timing_elapsed(self.h)
+
+    def kernel_ms(self, k: int) -> float:
+        return mw.mw_timing_kernel_ms(self.h, k)
+
+
+class Partition:
+    """Owns an mw_partition; exposes its streams as torch ExternalStreams."""
+
+    def __init__(self, prefill_cus: int, decode_cus: int, device: int = 0):
+        self.h = mw.mw_partition_create(device, prefill_cus, decode_cus)
+        self.prefill_stream, self.decode_stream = mw.mw_partition_streams(self.h)
+        self.prefill_cus, self.decode_cus = prefill_cus, decode_cus
+
+    def torch_streams(self):
+        return (torch.cuda.ExternalStream(self.prefill_stream),
+                torch.cuda.ExternalStream(self.decode_stream))
+
+    def masks(self):
+        return mw.mw_partition_masks(self.h)
+
+    def close(self):
+        if self.h is not None:
+            mw.mw_partition_destroy(self.h)
+            self.h = None

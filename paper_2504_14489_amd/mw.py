@@ -1,0 +1,304 @@
+"""Python binding of the C ABI in include/mw.h (argument marshalling only).
+
+Every function here has the name of the C entry point it calls and does no
+arithmetic of its own: device buffers are passed as integer addresses (for
+torch tensors, ``t.data_ptr()``), host arrays as numpy int32 arrays, streams
+as integer hipStream_t handles (``torch.cuda.current_stream().cuda_stream``).
+A failing call raises :class:`MWError` carrying the status and the library's
+error text.
+
+The library must have been built (``python -m paper_2504_14489_amd.build``);
+there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmw.so")
+
+MW_OK = 0
+MW_ERR_INVALID_ARG = -1
+MW_ERR_UNSUPPORTED = -2
+MW_ERR_OUT_OF_PAGES = -3
+MW_ERR_HIP = -4
+MW_ERR_NOT_READY = -5
+
+
+class MWError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"[{status}] {message}")
+        self.status = status
+        self.message = message
+
+
+class _PoolDesc(ctypes.Structure):
+    _fields_ = [("num_pages", ctypes.c_int32), ("page_size", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32)]
+
+
+class _AttnShape(ctypes.Structure):
+    _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("scale", ctypes.c_float)]
+
+
+_lib = None
+_P = ctypes.c_void_p
+_I = ctypes.c_int32
+_PI = ctypes.POINTER(ctypes.c_int32)
+_PU = ctypes.POINTER(ctypes.c_uint32)
+_PF = ctypes.POINTER(ctypes.c_float)
+
+_SIGNATURES = {
+    "mw_last_error": ([], ctypes.c_char_p),
+    "mw_version": ([], _I),
+    "mw_sync": ([_P], _I),
+    "mw_kv_pool_create": ([ctypes.POINTER(_PoolDesc), _P, _P, ctypes.POINTER(_P)], _I),
+    "mw_kv_pool_destroy": ([_P], _I),
+    "mw_kv_pool_set_free_order": ([_P, _PI, _I], _I),
+    "mw_kv_pool_alloc": ([_P, _I, _PI], _I),
+    "mw_kv_pool_free": ([_P, _PI, _I], _I),
+    "mw_kv_pool_num_free": ([_P, _PI], _I),
+    "mw_kv_pool_write": ([_P, _I, _PI, _PI, _P, _P, _P, _I, _P, _P, _P, _P], _I),
+    "mw_kv_pool_gather": ([_P, _P, _I, _P, _P, _P], _I),
+    "mw_partition_create": ([_I, _I, _I, ctypes.POINTER(_P)], _I),
+    "mw_partition_create_masks": ([_I, _PU, _PU, _I, ctypes.POINTER(_P)], _I),
+    "mw_partition_streams": ([_P, ctypes.POINTER(_P), ctypes.POINTER(_P)], _I),
+    "mw_partition_masks": ([_P, _PU, _PU], _I),
+    "mw_partition_destroy": ([_P], _I),
+    "mw_cu_probe": ([_I, _I, _P, _P], _I),
+    "mw_timing_create": ([ctypes.POINTER(_P)], _I),
+    "mw_timing_destroy": ([_P], _I),
+    "mw_timing_mark": ([_P, _P], _I),
+    "mw_timing_elapsed": ([_P, _PF, _PF], _I),
+    "mw_timing_kernels": ([_P, _PI], _I),
+    "mw_timing_kernel_ms": ([_P, _I, _PF], _I),
+    "mw_timing_offsets": ([_P, _P, _PF, _PF], _I),
+    "mw_prefill_attn": ([_P, ctypes.POINTER(_AttnShape), _I, _PI, _PI, _P, _P, _P, _I, _P, _P, _P,
+                         _P], _I),
+    "mw_decode_workspace_size": ([ctypes.POINTER(_AttnShape), _I, _PI, _I,
+                                  ctypes.POINTER(ctypes.c_size_t)], _I),
+    "mw_decode_attn": ([_P, ctypes.POINTER(_AttnShape), _I, _PI, _P, _P, _I, _P, _P, _P,
+                        ctypes.c_size_t, _I, _P, _P], _I),
+}
+
+EXPORTED = tuple(_SIGNATURES)
+
+
+def load(path: str = LIB_PATH):
+    """Loads libmw.so (raising if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is missing: build it with `python -m paper_2504_14489_amd.build`")
+        lib = ctypes.CDLL(path)
+        for name, (args, res) in _SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = lib
+    return _lib
+
+
+def _check(st: int):
+    if st != MW_OK:
+        raise MWError(st, mw_last_error())
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32).reshape(-1))
+
+
+def _pi(a: np.ndarray):
+    return a.ctypes.data_as(_PI)
+
+
+def _shape(hq: int, hkv: int, head_dim: int, scale: float) -> _AttnShape:
+    return _AttnShape(int(hq), int(hkv), int(head_dim), float(scale))
+
+
+def _h(x) -> Optional[int]:
+    """A handle or device address as an int (None stays NULL)."""
+    if x is None:
+        return None
+    if isinstance(x, ctypes.c_void_p):
+        return x.value
+    return int(x)
+
+
+# ------------------------------------------------------------------ misc ---
+def mw_last_error() -> str:
+    return load().mw_last_error().decode()
+
+
+def mw_version() -> int:
+    return load().mw_version()
+
+
+def mw_sync(stream=0):
+    _check(load().mw_sync(_h(stream)))
+
+
+# ------------------------------------------------------------------ pool ---
+def mw_kv_pool_create(num_pages: int, page_size: int, num_kv_heads: int, head_dim: int,
+                      d_k_pages: int, d_v_pages: int):
+    out = _P()
+    desc = _PoolDesc(num_pages, page_size, num_kv_heads, head_dim)
+    _check(load().mw_kv_pool_create(ctypes.byref(desc), _h(d_k_pages), _h(d_v_pages),
+                                    ctypes.byref(out)))
+    return out
+
+
+def mw_kv_pool_destroy(pool):
+    _check(load().mw_kv_pool_destroy(pool))
+
+
+def mw_kv_pool_set_free_order(pool, perm):
+    p = _i32(perm)
+    _check(load().mw_kv_pool_set_free_order(pool, _pi(p), len(p)))
+
+
+def mw_kv_pool_alloc(pool, n_pages: int) -> np.ndarray:
+    out = np.zeros(max(n_pages, 1), dtype=np.int32)
+    _check(load().mw_kv_pool_alloc(pool, n_pages, _pi(out)))
+    return out[:n_pages]
+
+
+def mw_kv_pool_free(pool, pages):
+    p = _i32(pages)
+    _check(load().mw_kv_pool_free(pool, _pi(p), len(p)))
+
+
+def mw_kv_pool_num_free(pool) -> int:
+    n = ctypes.c_int32()
+    _check(load().mw_kv_pool_num_free(pool, ctypes.byref(n)))
+    return n.value
+
+
+def mw_kv_pool_write(pool, new_lens, start_pos, d_qo_indptr: int, d_start_pos: int,
+                     d_block_table: int, bt_stride: int, d_k_new: int, d_v_new: int,
+                     stream=0, timing=None):
+    nl, sp = _i32(new_lens), _i32(start_pos)
+    _check(load().mw_kv_pool_write(pool, len(nl), _pi(nl), _pi(sp), _h(d_qo_indptr),
+                                   _h(d_start_pos), _h(d_block_table), bt_stride, _h(d_k_new),
+                                   _h(d_v_new), _h(stream), timing))
+
+
+def mw_kv_pool_gather(pool, d_block_table: int, n_tokens: int, d_k_out: int, d_v_out: int,
+                      stream=0):
+    _check(load().mw_kv_pool_gather(pool, _h(d_block_table), n_tokens, _h(d_k_out),
+                                    _h(d_v_out), _h(stream)))
+
+
+# ------------------------------------------------------------- partition ---
+def mw_partition_create(device: int, prefill_cus: int, decode_cus: int):
+    out = _P()
+    _check(load().mw_partition_create(device, prefill_cus, decode_cus, ctypes.byref(out)))
+    return out
+
+
+def mw_partition_create_masks(device: int, prefill_mask, decode_mask):
+    pm = np.ascontiguousarray(prefill_mask, dtype=np.uint32)
+    dm = np.ascontiguousarray(decode_mask, dtype=np.uint32)
+    assert len(pm) == len(dm)
+    out = _P()
+    _check(load().mw_partition_create_masks(device, pm.ctypes.data_as(_PU), dm.ctypes.data_as(_PU),
+                                            len(pm), ctypes.byref(out)))
+    return out
+
+
+def mw_partition_streams(part) -> Tuple[int, int]:
+    p, d = _P(), _P()
+    _check(load().mw_partition_streams(part, ctypes.byref(p), ctypes.byref(d)))
+    return p.value or 0, d.value or 0
+
+
+def mw_partition_masks(part) -> Tuple[np.ndarray, np.ndarray]:
+    pm = np.zeros(8, dtype=np.uint32)
+    dm = np.zeros(8, dtype=np.uint32)
+    _check(load().mw_partition_masks(part, pm.ctypes.data_as(_PU), dm.ctypes.data_as(_PU)))
+    return pm, dm
+
+
+def mw_partition_destroy(part):
+    _check(load().mw_partition_destroy(part))
+
+
+def mw_cu_probe(n_blocks: int, spin_cycles: int, d_out: int, stream=0):
+    _check(load().mw_cu_probe(n_blocks, spin_cycles, _h(d_out), _h(stream)))
+
+
+# ---------------------------------------------------------------- timing ---
+def mw_timing_create():
+    out = _P()
+    _check(load().mw_timing_create(ctypes.byref(out)))
+    return out
+
+
+def mw_timing_destroy(t):
+    _check(load().mw_timing_destroy(t))
+
+
+def mw_timing_mark(t, stream=0):
+    _check(load().mw_timing_mark(t, _h(stream)))
+
+
+def mw_timing_elapsed(t) -> Tuple[float, float]:
+    g, h = ctypes.c_float(), ctypes.c_float()
+    _check(load().mw_timing_elapsed(t, ctypes.byref(g), ctypes.byref(h)))
+    return g.value, h.value
+
+
+def mw_timing_kernels(t) -> int:
+    n = ctypes.c_int32()
+    _check(load().mw_timing_kernels(t, ctypes.byref(n)))
+    return n.value
+
+
+def mw_timing_kernel_ms(t, k: int) -> float:
+    ms = ctypes.c_float()
+    _check(load().mw_timing_kernel_ms(t, k, ctypes.byref(ms)))
+    return ms.value
+
+
+def mw_timing_offsets(t, ref) -> Tuple[float, float]:
+    a, b = ctypes.c_float(), ctypes.c_float()
+    _check(load().mw_timing_offsets(t, ref, ctypes.byref(a), ctypes.byref(b)))
+    return a.value, b.value
+
+
+# ------------------------------------------------------------- attention ---
+def mw_prefill_attn(pool, num_q_heads: int, num_kv_heads: int, head_dim: int, scale: float,
+                    new_lens, prefix_lens, d_qo_indptr: int, d_prefix_lens: int,
+                    d_block_table: int, bt_stride: int, d_q: int, d_out: int, stream=0,
+                    timing=None):
+    nl, pl = _i32(new_lens), _i32(prefix_lens)
+    sh = _shape(num_q_heads, num_kv_heads, head_dim, scale)
+    _check(load().mw_prefill_attn(pool, ctypes.byref(sh), len(nl), _pi(nl), _pi(pl),
+                                  _h(d_qo_indptr), _h(d_prefix_lens), _h(d_block_table), bt_stride,
+                                  _h(d_q), _h(d_out), _h(stream), timing))
+
+
+def mw_decode_workspace_size(num_q_heads: int, num_kv_heads: int, head_dim: int, seq_lens,
+                             chunk_pages: int = 0) -> int:
+    sl = _i32(seq_lens)
+    sh = _shape(num_q_heads, num_kv_heads, head_dim, 1.0)
+    out = ctypes.c_size_t()
+    _check(load().mw_decode_workspace_size(ctypes.byref(sh), len(sl), _pi(sl), chunk_pages,
+                                           ctypes.byref(out)))
+    return out.value
+
+
+def mw_decode_attn(pool, num_q_heads: int, num_kv_heads: int, head_dim: int, scale: float,
+                   seq_lens, d_seq_lens: int, d_block_table: int, bt_stride: int, d_q: int,
+                   d_out: int, d_workspace: int, workspace_bytes: int, chunk_pages: int = 0,
+                   stream=0, timing=None):
+    sl = _i32(seq_lens)
+    sh = _shape(num_q_heads, num_kv_heads, head_dim, scale)
+    _check(load().mw_decode_attn(pool, ctypes.byref(sh), len(sl), _pi(sl), _h(d_seq_lens),
+                                 _h(d_block_table), bt_stride, _h(d_q), _h(d_out), _h(d_workspace),
+                                 workspace_bytes, chunk_pages, _h(stream), timing))

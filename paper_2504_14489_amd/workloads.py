@@ -27,12 +27,17 @@ Poison (so that a kernel reading what it must not read fails parity):
   one dominates the softmax).
 
 Draw order from ``numpy.random.Generator(PCG64(seed))``: decode lengths, page
-permutation, prefill Q, decode Q, K, V.
+permutation, prefill Q, decode Q.  K and V are drawn per block of 1024 pages,
+block j of K from ``PCG64(SeedSequence([seed, 1, j]))`` and of V from
+``PCG64(SeedSequence([seed, 2, j]))``, so that blocks can be drawn in
+parallel.
 """
 from __future__ import annotations
 
+import concurrent.futures
 import dataclasses
 import math
+import os
 from typing import List, Optional, Tuple
 
 import numpy as np
@@ -193,6 +198,27 @@ def draw_decode_lengths(cfg: Config, rng: np.random.Generator) -> np.ndarray:
     return L.astype(np.int32)
 
 
+_PAGE_BLOCK = 1024
+
+
+def _pool_bf16(seed: int, stream: int, shape) -> np.ndarray:
+    """N(0,1) bf16 pool [P][...]: page block j from its own seeded stream."""
+    P = shape[0]
+    out = np.empty(shape, dtype=np.uint16)
+
+    def fill(j):
+        g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, stream, j])))
+        lo, hi = j * _PAGE_BLOCK, min(P, (j + 1) * _PAGE_BLOCK)
+        x = g.standard_normal(size=(hi - lo,) + tuple(shape[1:]), dtype=np.float32)
+        out[lo:hi] = f32_to_bf16_bits(x)
+
+    blocks = range(-(-P // _PAGE_BLOCK))
+    workers = max(1, min(16, os.cpu_count() or 1))
+    with concurrent.futures.ThreadPoolExecutor(workers) as ex:
+        list(ex.map(fill, blocks))
+    return out
+
+
 def _normal_bf16(rng: np.random.Generator, shape, scale: float = 1.0) -> np.ndarray:
     x = rng.standard_normal(size=shape, dtype=np.float32)
     if scale != 1.0:
@@ -242,8 +268,8 @@ def make_workload(cfg: Config, seed: Optional[int] = None, q_scale: float = 1.0,
 
     q_pre = _normal_bf16(rng, (pre_len, Hq, D), q_scale)
     q_dec = _normal_bf16(rng, (B, Hq, D), q_scale)
-    k_pool = _normal_bf16(rng, (P, Hkv, S, D))
-    v_pool = _normal_bf16(rng, (P, Hkv, S, D))
+    k_pool = _pool_bf16(seed, 1, (P, Hkv, S, D))
+    v_pool = _pool_bf16(seed, 2, (P, Hkv, S, D))
 
     # poison: every page not dealt to a sequence is NaN (incl. the NaN page)
     used = np.zeros(P, dtype=bool)

@@ -1,0 +1,102 @@
+"""Decode attention on the GPU against the CPU oracle (same seeded inputs)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2504_14489_amd import workloads as W
+from paper_2504_14489_amd.device import DeviceWorkload, to_bits
+from tests.helpers import assert_close, say
+
+pytestmark = pytest.mark.gpu
+
+# lengths on and around page and chunk boundaries (16-token pages, 4..16-page chunks)
+EDGE_LENS = [1, 2, 15, 16, 17, 63, 64, 65, 255, 256, 257, 1000, 1023, 1024, 1025, 4097]
+
+
+def run_decode(wl, chunk_pages=0, q_scale=None):
+    dw = DeviceWorkload(wl)
+    try:
+        o = dw.decode(chunk_pages=chunk_pages)
+        torch.cuda.synchronize()
+        return to_bits(o)
+    finally:
+        dw.close()
+
+
+@pytest.mark.parametrize("hq,hkv", [(8, 2), (32, 8), (64, 8), (4, 4), (16, 1), (6, 2)])
+@pytest.mark.parametrize("q_scale", [1.0, 4.0])
+def test_decode_matches_oracle_on_edge_lengths(hq, hkv, q_scale):
+    say(f"decode hq={hq} hkv={hkv} q_scale={q_scale}")
+    cfg = W.custom_config(hq=hq, hkv=hkv, pre_chunks=((0, 1),), dec_batch=len(EDGE_LENS),
+                          seed=hq + hkv)
+    wl = W.make_workload(cfg, q_scale=q_scale, dec_lens=EDGE_LENS)
+    got = run_decode(wl)
+    ref = oracle.decode(wl.q_dec, wl.k_pool, wl.v_pool, wl.dec_bt, wl.dec_lens)
+    assert_close(got, ref, f"decode hq={hq} hkv={hkv}")
+
+
+@pytest.mark.parametrize("chunk_pages", [4, 8, 16])
+def test_decode_split_count_invariance(chunk_pages):
+    say(f"decode chunk_pages={chunk_pages}")
+    cfg = W.custom_config(hq=32, hkv=8, pre_chunks=((0, 1),), dec_batch=12, dec_len_lo=1,
+                          dec_len_hi=3000, seed=21)
+    wl = W.make_workload(cfg)
+    got = run_decode(wl, chunk_pages)
+    ref = oracle.decode(wl.q_dec, wl.k_pool, wl.v_pool, wl.dec_bt, wl.dec_lens)
+    assert_close(got, ref, f"decode chunk_pages={chunk_pages}")
+
+
+def test_decode_tiny_config_full_parity():
+    say("decode tiny config")
+    wl = W.make_workload(W.CONFIGS["tiny"])
+    got = run_decode(wl)
+    ref = oracle.decode(wl.q_dec, wl.k_pool, wl.v_pool, wl.dec_bt, wl.dec_lens)
+    assert_close(got, ref, "decode tiny")
+
+
+def test_decode_page_permutation_invariance_and_determinism():
+    say("decode permutation invariance")
+    cfg = W.custom_config(hq=8, hkv=2, pre_chunks=((0, 1),), dec_batch=9, dec_len_lo=1,
+                          dec_len_hi=900, seed=33)
+    wl = W.make_workload(cfg)
+    a = run_decode(wl)
+    b = run_decode(wl)
+    assert np.array_equal(a, b), "run-to-run results differ"
+    rng = np.random.default_rng(4)
+    new_of_old = rng.permutation(wl.num_pages).astype(np.int32)
+    k = np.empty_like(wl.k_pool); k[new_of_old] = wl.k_pool
+    v = np.empty_like(wl.v_pool); v[new_of_old] = wl.v_pool
+    wl2 = W.Workload(cfg=wl.cfg, k_pool=k, v_pool=v, nan_page=int(new_of_old[wl.nan_page]),
+                     pre_len=wl.pre_len, pre_bt=new_of_old[wl.pre_bt], q_pre=wl.q_pre,
+                     dec_lens=wl.dec_lens, dec_bt=new_of_old[wl.dec_bt], q_dec=wl.q_dec,
+                     perm=wl.perm)
+    c = run_decode(wl2)
+    assert np.array_equal(a, c), "page renumbering changed the result"
+
+
+def test_decode_equals_last_prefill_row():
+    say("decode vs last prefill row")
+    from paper_2504_14489_amd.device import DeviceWorkload as DW
+    cfg = W.custom_config(hq=8, hkv=2, pre_chunks=((0, 77),), dec_batch=1, dec_len_lo=1,
+                          dec_len_hi=2, seed=8)
+    wl = W.make_workload(cfg)
+    dw = DW(wl)
+    try:
+        pre = to_bits(dw.prefill(0, 77))[-1]
+        # decode the last prefill token over the same 77-token sequence
+        dw.q_dec = dw.q_pre[76:77].contiguous()
+        dw.dec_bt = dw.pre_bt
+        dw.dec_lens = np.array([77], np.int32)
+        dw.d_dec_lens = torch.tensor([77], dtype=torch.int32, device=dw.device)
+        dw.o_dec = torch.zeros_like(dw.q_dec)
+        dw._ws.clear()
+        dec = to_bits(dw.decode())[0]
+        torch.cuda.synchronize()
+    finally:
+        dw.close()
+    ref = oracle.prefill(wl.q_pre[76:77], wl.k_pool, wl.v_pool, wl.pre_bt, 76)[0]
+    assert_close(pre[None], ref[None], "prefill last row")
+    assert_close(dec[None], ref[None], "decode")
+    diff = np.abs(W.bf16_bits_to_f32(pre) - W.bf16_bits_to_f32(dec))
+    assert diff.max() <= 2e-2

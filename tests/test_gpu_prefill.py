@@ -1,0 +1,121 @@
+"""Causal prefill attention on the GPU against the CPU oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2504_14489_amd import workloads as W
+from paper_2504_14489_amd.device import DeviceWorkload, to_bits
+from tests.helpers import assert_close, say
+
+pytestmark = pytest.mark.gpu
+
+# (prefix r, new n): empty prefix, single token, tile and page boundaries, ragged tails
+CHUNKS = [(0, 1), (0, 63), (0, 64), (0, 65), (5, 100), (33, 17), (100, 130), (0, 256),
+          (64, 64), (1, 200)]
+
+
+def run_prefill(wl, r, n):
+    dw = DeviceWorkload(wl)
+    try:
+        o = dw.prefill(r, n)
+        torch.cuda.synchronize()
+        return to_bits(o)
+    finally:
+        dw.close()
+
+
+@pytest.mark.parametrize("hq,hkv", [(8, 2), (64, 8), (4, 4), (2, 1), (12, 2)])
+@pytest.mark.parametrize("q_scale", [1.0, 4.0])
+def test_prefill_matches_oracle(hq, hkv, q_scale):
+    for r, n in CHUNKS:
+        say(f"prefill hq={hq} hkv={hkv} r={r} n={n} q_scale={q_scale}")
+        cfg = W.custom_config(hq=hq, hkv=hkv, pre_chunks=((r, n),), dec_batch=1, dec_len_lo=1,
+                              dec_len_hi=2, seed=r * 7 + n)
+        wl = W.make_workload(cfg, q_scale=q_scale)
+        got = run_prefill(wl, r, n)
+        ref = oracle.prefill(wl.q_pre[r:r + n], wl.k_pool, wl.v_pool, wl.pre_bt, r)
+        assert_close(got, ref, f"prefill hq={hq} hkv={hkv} r={r} n={n}")
+
+
+def test_prefill_tiny_config_full_parity():
+    say("prefill tiny config")
+    wl = W.make_workload(W.CONFIGS["tiny"])
+    got = run_prefill(wl, 0, 256)
+    ref = oracle.prefill(wl.q_pre[:256], wl.k_pool, wl.v_pool, wl.pre_bt, 0)
+    assert_close(got, ref, "prefill tiny")
+
+
+def test_chunked_prefill_matches_unchunked():
+    say("prefill chunked vs unchunked")
+    cfg = W.custom_config(hq=8, hkv=2, pre_chunks=((0, 300),), dec_batch=1, dec_len_lo=1,
+                          dec_len_hi=2, seed=3)
+    wl = W.make_workload(cfg)
+    dw = DeviceWorkload(wl)
+    try:
+        full = to_bits(dw.prefill(0, 300).clone())
+        parts = [to_bits(dw.prefill(r, n).clone()) for r, n in ((0, 100), (100, 77), (177, 123))]
+        torch.cuda.synchronize()
+    finally:
+        dw.close()
+    chunked = np.concatenate(parts)
+    ref = oracle.prefill(wl.q_pre[:300], wl.k_pool, wl.v_pool, wl.pre_bt, 0)
+    assert_close(full, ref, "unchunked")
+    assert_close(chunked, ref, "chunked")
+
+
+def test_prefill_page_permutation_invariance_and_determinism():
+    say("prefill permutation invariance")
+    cfg = W.custom_config(hq=8, hkv=2, pre_chunks=((40, 150),), dec_batch=1, dec_len_lo=1,
+                          dec_len_hi=2, seed=9)
+    wl = W.make_workload(cfg)
+    a = run_prefill(wl, 40, 150)
+    assert np.array_equal(a, run_prefill(wl, 40, 150)), "run-to-run results differ"
+    rng = np.random.default_rng(5)
+    new_of_old = rng.permutation(wl.num_pages).astype(np.int32)
+    k = np.empty_like(wl.k_pool); k[new_of_old] = wl.k_pool
+    v = np.empty_like(wl.v_pool); v[new_of_old] = wl.v_pool
+    wl2 = W.Workload(cfg=wl.cfg, k_pool=k, v_pool=v, nan_page=int(new_of_old[wl.nan_page]),
+                     pre_len=wl.pre_len, pre_bt=new_of_old[wl.pre_bt], q_pre=wl.q_pre,
+                     dec_lens=wl.dec_lens, dec_bt=new_of_old[wl.dec_bt], q_dec=wl.q_dec,
+                     perm=wl.perm)
+    assert np.array_equal(a, run_prefill(wl2, 40, 150)), "page renumbering changed the result"
+
+
+def test_prefill_varlen_batch():
+    """Three sequences in one call (block-table rows, varlen Q/O offsets)."""
+    say("prefill varlen batch")
+    from paper_2504_14489_amd import mw
+    seqs = [(0, 70), (20, 5), (130, 64)]
+    cfgs = [W.custom_config(hq=8, hkv=2, pre_chunks=((r, n),), dec_batch=1, dec_len_lo=1,
+                            dec_len_hi=2, seed=40 + i) for i, (r, n) in enumerate(seqs)]
+    wls = [W.make_workload(c) for c in cfgs]
+    # one pool holding all three sequences: concatenate pools and offset their tables
+    k = np.concatenate([w.k_pool for w in wls]); v = np.concatenate([w.v_pool for w in wls])
+    offs = np.cumsum([0] + [w.num_pages for w in wls])
+    stride = max(len(w.pre_bt) for w in wls)
+    bt = np.full((3, stride), 0, np.int32)
+    for i, w in enumerate(wls):
+        bt[i, :len(w.pre_bt)] = w.pre_bt + offs[i]
+    q = np.concatenate([w.q_pre[r:r + n] for w, (r, n) in zip(wls, seqs)])
+    dev = torch.device("cuda:0")
+    t16 = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev)
+    t32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
+    dk, dv, dq, dbt = t16(k), t16(v), t16(q), t32(bt)
+    do = torch.zeros_like(dq)
+    indptr = t32(np.cumsum([0] + [n for _, n in seqs]))
+    pref = t32([r for r, _ in seqs])
+    pool = mw.mw_kv_pool_create(k.shape[0], 16, 2, 128, dk.data_ptr(), dv.data_ptr())
+    try:
+        mw.mw_prefill_attn(pool, 8, 2, 128, 1 / np.sqrt(128), [n for _, n in seqs],
+                           [r for r, _ in seqs], indptr.data_ptr(), pref.data_ptr(),
+                           dbt.data_ptr(), stride, dq.data_ptr(), do.data_ptr())
+        torch.cuda.synchronize()
+    finally:
+        mw.mw_kv_pool_destroy(pool)
+    got = to_bits(do)
+    row = 0
+    for w, (r, n) in zip(wls, seqs):
+        ref = oracle.prefill(w.q_pre[r:r + n], w.k_pool, w.v_pool, w.pre_bt, r)
+        assert_close(got[row:row + n], ref, f"varlen seq r={r} n={n}")
+        row += n
