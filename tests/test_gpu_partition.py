@@ -18,8 +18,10 @@ def cu_ids(raw: np.ndarray):
     return np.stack([xcc, (hw >> 13) & 0x7, (hw >> 12) & 0x1, (hw >> 8) & 0xF], axis=1)
 
 
-def probe(stream: int, n_blocks: int, spin: int) -> torch.Tensor:
-    out = torch.zeros(4 * n_blocks, dtype=torch.int32, device="cuda:0")
+def probe(stream: int, n_blocks: int, spin: int, out=None) -> torch.Tensor:
+    if out is None:
+        out = torch.zeros(4 * n_blocks, dtype=torch.int32, device="cuda:0")
+        torch.cuda.synchronize()
     mw.mw_cu_probe(n_blocks, spin, out.data_ptr(), stream)
     return out
 
@@ -51,9 +53,14 @@ def test_partition_masks_select_disjoint_cus_evenly_over_xcds(p_cus, d_cus):
 def test_partition_streams_run_concurrently():
     say("partition concurrency")
     part = Partition(128, 128)
+    # buffers first: work on the null stream would serialise with both
+    # (blocking) partition streams
+    d = torch.zeros(4 * 8192, dtype=torch.int32, device="cuda:0")
+    p = torch.zeros_like(d)
+    torch.cuda.synchronize()
     try:
-        d = probe(part.decode_stream, 8192, 40000)
-        p = probe(part.prefill_stream, 8192, 40000)
+        probe(part.decode_stream, 8192, 400000, d)
+        probe(part.prefill_stream, 8192, 400000, p)
         torch.cuda.synchronize()
         rd = d.cpu().numpy().astype(np.uint32).reshape(-1, 4).astype(np.int64)
         rp = p.cpu().numpy().astype(np.uint32).reshape(-1, 4).astype(np.int64)
