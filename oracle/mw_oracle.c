@@ -263,8 +263,8 @@ int32_t mwo_partial(int32_t hq, int32_t hkv, int32_t d, int32_t s, double scale,
         for (int32_t e = 0; e < d; ++e) dot += bf16_to_double(q[e]) * bf16_to_double(k[e]);
         sc[j - j0] = dot * scale;
     }
-    double m = sc[0];
-    for (int32_t j = 1; j < j1 - j0; ++j)
+    double m = -INFINITY;
+    for (int32_t j = 0; j < j1 - j0; ++j)
         if (sc[j] > m) m = sc[j];
     double l = 0.0;
     for (int32_t j = j0; j < j1; ++j) {
