@@ -43,8 +43,8 @@
  *     Q and O       : [tokens][num_q_heads][head_dim] bf16.
  *   Query head h reads KV head h / (num_q_heads / num_kv_heads).
  * - Device-side page indices outside [0, num_pages) are never dereferenced:
- *   kernels treat such a page as zeros (results are then meaningless, but no
- *   memory outside the pool is touched).
+ *   kernels treat such a page as zeros or as absent (results are then
+ *   meaningless, but no memory outside the pool is touched).
  * - Asynchronous HIP faults surface as MW_ERR_HIP from the next call that
  *   synchronises (mw_timing_elapsed, mw_sync), with the HIP error text in
  *   mw_last_error().
@@ -222,8 +222,9 @@ mw_status mw_prefill_attn(const mw_kv_pool *pool, const mw_attn_shape *shape, in
                           const int32_t *d_block_table, int32_t bt_stride, const void *d_q,
                           void *d_out, mw_stream stream, mw_timing *timing);
 
-/* Decode is split over chunks of `chunk_pages` pages of each sequence
- * (0 = default 16) and merged by a second kernel (log-sum-exp combine).  The
+/* Decode is split over chunks of `chunk_pages` pages of each sequence (a
+ * multiple of 8 in [8, 256]; 0 = default 32) and merged by a second kernel
+ * (log-sum-exp combine).  The
  * split depends only on the lengths, never on page ids.
  * Workspace bytes for a call with these lengths: */
 mw_status mw_decode_workspace_size(const mw_attn_shape *shape, int32_t batch,

@@ -3,29 +3,29 @@
 // Decode is memory-bound (paper Sec. 2.2: the decode phase is
 // memory-intensive; Sec. 3.3, Table "tab:theory_cost": O(d^2 + (r+1) d)), so
 // the design goal is streaming every K/V byte of the batch from HBM exactly
-// once with enough bytes in flight, not arithmetic throughput.
+// once with enough bytes in flight; arithmetic is kept off the vector ALU.
 //
-// Work unit = (sequence b, kv head, chunk of CH consecutive pages).  The split
-// depends only on the sequence lengths (never on page ids), so a result does
-// not change when pages are renumbered.
+// Work-group = (sequence b, kv head, chunk of CH consecutive pages), 4 waves.
+// The split depends only on the sequence lengths (never on page ids), so a
+// result does not change when pages are renumbered.
 //
-// Per unit (4 waves, PPW = CH/4 pages per wave):
-//   1. All K and V page rows of the wave are loaded up front (16-byte vector
-//      loads; every lane has 16 loads of 16 B in flight per page pair).
-//   2. Scores of the chunk's tokens against the G query heads of the kv head
-//      come from one 16x16x32 bf16 MFMA per 32 dims: A = the page's K rows
-//      [16 tokens x 32 dims] exactly as loaded from HBM, B = Q^T for the
-//      group's heads (columns >= G are zero).  The MFMA is used only because
-//      it reads K in its memory layout with no shuffles.
-//   3. Max and sum over the chunk (per head) use cross-lane shuffles and a
-//      4-entry LDS exchange; p = exp2(s*scale*log2e - m) stays in registers
-//      and goes to LDS once for the value pass.
-//   4. p*V on the vector ALU in fp32: each lane owns 8 dims of 4 tokens of a
-//      page, so each V load instruction reads 4 whole 256-byte token rows.
-//   5. Partials (m, l, unnormalised o) go to the workspace; a sequence with a
-//      single chunk writes its normalised bf16 output directly.
-// The combine kernel merges the chunks of each (sequence, kv head) with the
-// log-sum-exp identity: M = max m_s, O = sum 2^(m_s-M) o_s / sum 2^(m_s-M) l_s.
+// Each wave streams its own pages of the chunk two at a time (a "pair"), with
+// the next pair's loads in flight while the current pair is computed:
+//   * K rows are loaded straight into the A operand of a 16x16x32 bf16 MFMA
+//     (one page = 16 tokens x 32 dims per step), B = Q^T of the kv head's G
+//     query heads (columns >= G are zero): S^T[token][head].
+//   * V rows go to a per-wave LDS buffer as loaded (16-byte row-major stores)
+//     and come back through the transposing LDS read as the A operand of a
+//     second MFMA, O^T[d][head] += V^T[d][token] P^T[token][head]; P^T is the
+//     S^T accumulator itself, converted to bf16.
+//   * online softmax per pair in base 2; the reference maximum moves only
+//     when a column's maximum grows by more than 2^8 (O and l are then
+//     rescaled), which the result O / l does not depend on.
+// The 4 waves' (m, l, O) are merged in LDS at the end; a sequence that fits
+// one chunk writes its bf16 output directly, otherwise the chunk's partial goes
+// to the workspace and the combine kernel merges the chunks of each
+// (sequence, kv head) with the log-sum-exp identity
+//   M = max m_s,  O = sum 2^(m_s - M) o_s / sum 2^(m_s - M) l_s.
 #include "mw_internal.h"
 
 using namespace mw;
@@ -33,15 +33,33 @@ using namespace mw;
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
+constexpr int kPair = 2;                      // pages per wave step
+constexpr int VSTR = 144;                     // LDS V row stride (bf16): conflict-free
+constexpr int kVBufElems = 16 * kPair * VSTR; // one wave's V buffer
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kRescaleLog2 = 8.f;
+constexpr int kDefaultChunkPages = 32;
 
-__device__ inline float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ inline float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 __device__ inline uint16_t to_bf16(float f) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f)); }
+__device__ inline uint32_t cvt2(float a, float b) {
+    bf16x2 v;
+    v[0] = static_cast<__bf16>(a);
+    v[1] = static_cast<__bf16>(b);
+    return __builtin_bit_cast(uint32_t, v);
+}
+__device__ inline uint4 sel4(bool ok, uint4 v) {
+    return make_uint4(ok ? v.x : 0u, ok ? v.y : 0u, ok ? v.z : 0u, ok ? v.w : 0u);
+}
+__device__ inline i16x4 lds_read_tr(const uint16_t *p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        reinterpret_cast<__attribute__((address_space(3))) i16x4 *>(reinterpret_cast<uintptr_t>(p)));
+}
 
 __device__ inline int chunks_of(int L, int ch_pages, int bt_stride) {
     if (L <= 0) return 0;
@@ -50,208 +68,220 @@ __device__ inline int chunks_of(int L, int ch_pages, int bt_stride) {
     return (np + ch_pages - 1) / ch_pages;
 }
 
-// Block-wide search for the sequence b and chunk c holding global chunk ci.
-// s_loc = {b (or -1), c, first chunk index of b, chunks of b}.
-__device__ void locate_chunk(const int32_t *__restrict__ seq_lens, int batch, int ch_pages,
-                             int bt_stride, int ci, int *s_loc, int *s_wsum) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    if (threadIdx.x == 0) s_loc[0] = -1;
-    __syncthreads();
+// Wave-level search for the sequence b and chunk c holding global chunk ci
+// (every wave runs it; no barrier).  Returns false if ci is past the end.
+__device__ bool locate_chunk(const int32_t *__restrict__ seq_lens, int batch, int ch_pages, int bt_stride,
+                             int ci, int &b_out, int &c_out, int &nch_out, int &first_out) {
+    const int lane = threadIdx.x & 63;
     int running = 0;
-    for (int base = 0; base < batch; base += kThreads) {
-        const int b = base + threadIdx.x;
-        const int n = b < batch ? chunks_of(seq_lens[b], ch_pages, bt_stride) : 0;
+    for (int base = 0; base < batch; base += 64) {
+        const int bb = base + lane;
+        const int n = bb < batch ? chunks_of(seq_lens[bb], ch_pages, bt_stride) : 0;
         int x = n;
+#pragma unroll
         for (int off = 1; off < 64; off <<= 1) {
             const int y = __shfl_up(x, off);
             if (lane >= off) x += y;
         }
-        if (lane == 63) s_wsum[wave] = x;
-        __syncthreads();
-        int wbase = 0, total = 0;
-        for (int w = 0; w < kWaves; ++w) {
-            const int v = s_wsum[w];
-            total += v;
-            if (w < wave) wbase += v;
+        const int incl = running + x, excl = incl - n;
+        const uint64_t hit = __builtin_amdgcn_ballot_w64(bb < batch && ci >= excl && ci < incl);
+        if (hit) {
+            const int src = __builtin_ctzll(hit);
+            first_out = __shfl(excl, src);
+            b_out = base + src;
+            c_out = ci - first_out;
+            nch_out = __shfl(n, src);
+            return true;
         }
-        const int incl = running + wbase + x, excl = incl - n;
-        if (b < batch && ci >= excl && ci < incl) {
-            s_loc[0] = b;
-            s_loc[1] = ci - excl;
-            s_loc[2] = excl;
-            s_loc[3] = n;
-        }
-        running += total;
-        __syncthreads();
+        running = __shfl(incl, 63);
+    }
+    return false;
+}
+
+struct PairRegs {
+    uint4 k[kPair][4];  // K rows as the MFMA A operand: token = lane%16, dims 32kb + 8(lane/16) + 0..7
+    uint4 v[kPair][4];  // V rows: token 4i + lane/16, dims 8(lane%16) + 0..7
+    bool ok[kPair];
+};
+
+__device__ inline void pair_load(PairRegs &pr, const uint16_t *__restrict__ kpool,
+                                 const uint16_t *__restrict__ vpool, const int32_t *__restrict__ btrow,
+                                 int p0, int p_end, int hkv, int kvh, int num_pages) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int j = 0; j < kPair; ++j) {
+        const int p = p0 + j;
+        const int page = btrow[p < p_end ? p : p0];
+        pr.ok[j] = p < p_end && page >= 0 && page < num_pages;
+        const size_t base = (static_cast<size_t>(pr.ok[j] ? page : 0) * hkv + kvh) * (kPageSize * kHeadDim);
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+            pr.k[j][kb] = *reinterpret_cast<const uint4 *>(kpool + base + (lane & 15) * kHeadDim + 32 * kb +
+                                                          8 * (lane >> 4));
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            pr.v[j][i] = *reinterpret_cast<const uint4 *>(vpool + base + (4 * i + (lane >> 4)) * kHeadDim +
+                                                         8 * (lane & 15));
     }
 }
 
-template <int GP, int PPW>
 __global__ void __launch_bounds__(kThreads)
 k_decode_split(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpool,
                const uint16_t *__restrict__ q, uint16_t *__restrict__ out,
                const int32_t *__restrict__ seq_lens, const int32_t *__restrict__ bt, int bt_stride,
                float *__restrict__ ws_o, float2 *__restrict__ ws_ml, int32_t *__restrict__ ws_cbase,
-               int batch, int hkv, int group, int num_pages, float scale_log2) {
-    constexpr int CH = kWaves * PPW;
-    constexpr int kPBytes = CH * 16 * 16 * 4;            // p per [page][token][head]
-    constexpr int kOBytes = kWaves * GP * kHeadDim * 4;  // per-wave partial o
-    constexpr int kScratch = kPBytes > kOBytes ? kPBytes : kOBytes;
-    __shared__ int s_loc[4];
-    __shared__ int s_wsum[kWaves];
-    __shared__ float s_red[kWaves][16];
-    __shared__ float s_ml[2][16];
-    __shared__ __attribute__((aligned(16))) float s_buf[kScratch / 4];
+               int batch, int hkv, int group, int num_pages, float scale_log2, int ch_pages) {
+    __shared__ __attribute__((aligned(16))) uint16_t s_v[kWaves * kVBufElems];
+    __shared__ float s_m[kWaves][16];
+    __shared__ float s_l[kWaves][16];
 
     const int u = blockIdx.x;
     const int kvh = u % hkv;
-    locate_chunk(seq_lens, batch, CH, bt_stride, u / hkv, s_loc, s_wsum);
-    const int b = s_loc[0];
-    if (b < 0) return;  // more units launched than the device lengths give
-    const int c = s_loc[1];
-    const int nch = s_loc[3];
+    int b, c, nch, first;
+    if (!locate_chunk(seq_lens, batch, ch_pages, bt_stride, u / hkv, b, c, nch, first))
+        return;  // more units launched than the device lengths give (uniform over the block)
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int col = lane & 15, grp = lane >> 4;
     const int L = min(seq_lens[b], bt_stride * kPageSize);
     const int np_b = (L + kPageSize - 1) / kPageSize;
-    const int p_begin = c * CH;
-    const int p_end = min(p_begin + CH, np_b);
+    const int p_end = min((c + 1) * ch_pages, np_b);
     const int32_t *btrow = bt + static_cast<size_t>(b) * bt_stride;
     const int hq = hkv * group;
-    const uint4 zero4 = make_uint4(0, 0, 0, 0);
 
-    // ---- issue every load of this wave: K (MFMA A layout) and V (row layout)
-    uint4 kr[PPW][4], vr[PPW][4];
-    bool pin[PPW];
-#pragma unroll
-    for (int i = 0; i < PPW; ++i) {
-        const int p = p_begin + wave + kWaves * i;
-        pin[i] = p < p_end;
-        const int page = pin[i] ? btrow[p] : -1;
-        const bool ok = page >= 0 && page < num_pages;
-        const size_t base = (static_cast<size_t>(ok ? page : 0) * hkv + kvh) * (kPageSize * kHeadDim);
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-            kr[i][kb] = ok ? *reinterpret_cast<const uint4 *>(kpool + base + col * kHeadDim + 32 * kb + 8 * grp)
-                           : zero4;
-#pragma unroll
-        for (int t4 = 0; t4 < 4; ++t4)
-            vr[i][t4] = ok ? *reinterpret_cast<const uint4 *>(vpool + base + (4 * grp + t4) * kHeadDim + 8 * col)
-                           : zero4;
-    }
-
-    // ---- Q^T operand: column `col` is query head kvh*group + col
+    // Q^T operand: column `col` is query head kvh*group + col
     uint4 qop[4];
     {
         const bool hv = col < group;
         const uint16_t *qp = q + (static_cast<size_t>(b) * hq + kvh * group + (hv ? col : 0)) * kHeadDim + 8 * grp;
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) qop[kb] = hv ? *reinterpret_cast<const uint4 *>(qp + 32 * kb) : zero4;
+        for (int kb = 0; kb < 4; ++kb)
+            qop[kb] = hv ? *reinterpret_cast<const uint4 *>(qp + 32 * kb) : make_uint4(0, 0, 0, 0);
     }
 
-    // ---- scores: S^T[token][head], lane holds tokens 4*grp+r of head `col`
-    f32x4 s[PPW];
-    float mx = -INFINITY;
+    f32x4 oacc[8];  // O^T[d = 16db + 4grp + i][head = col]
 #pragma unroll
-    for (int i = 0; i < PPW; ++i) {
-        s[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-        if (pin[i]) {
+    for (int db = 0; db < 8; ++db) oacc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m_run = -INFINITY, l_run = 0.f;
+
+    uint16_t *vbuf = s_v + wave * kVBufElems;
+    // transposing-read source: lane s of 16-lane group g -> row 4g + s/4 (+16 for
+    // the second page), dims 4(s%4) (+16 db)
+    const uint16_t *vtr = vbuf + (4 * grp + (col >> 2)) * VSTR + 4 * (col & 3);
+
+    // this wave's pairs: pages c*CH + 2*(wave + 4*j) + {0, 1}
+    const int pstart = c * ch_pages + kPair * wave;
+    const int pstep = kPair * kWaves;
+    PairRegs pr;
+    if (pstart < p_end) pair_load(pr, kpool, vpool, btrow, pstart, p_end, hkv, kvh, num_pages);
+    for (int p0 = pstart; p0 < p_end; p0 += pstep) {
+        bool ok[kPair];
+#pragma unroll
+        for (int j = 0; j < kPair; ++j) ok[j] = pr.ok[j];
+        // V of this pair -> LDS (as loaded; an absent page as zeros), then
+        // K -> S^T on the matrix core (scores of an absent page are masked)
+#pragma unroll
+        for (int j = 0; j < kPair; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                *reinterpret_cast<uint4 *>(vbuf + (16 * j + 4 * i + grp) * VSTR + 8 * col) = sel4(pr.ok[j], pr.v[j][i]);
+        f32x4 sc[kPair];
+#pragma unroll
+        for (int j = 0; j < kPair; ++j) {
+            sc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb)
-                s[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[i][kb]),
-                                                               __builtin_bit_cast(bf16x8, qop[kb]), s[i], 0, 0, 0);
+                sc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, pr.k[j][kb]),
+                                                                __builtin_bit_cast(bf16x8, qop[kb]), sc[j], 0, 0, 0);
         }
-        const int tok0 = (p_begin + wave + kWaves * i) * kPageSize + 4 * grp;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const float v = (pin[i] && tok0 + r < L) ? s[i][r] * scale_log2 : -INFINITY;
-            s[i][r] = v;
-            mx = fmaxf(mx, v);
-        }
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    if (grp == 0) s_red[wave][col] = mx;
-    __syncthreads();
-    const float m = fmaxf(fmaxf(s_red[0][col], s_red[1][col]), fmaxf(s_red[2][col], s_red[3][col]));
+        // next pair's loads go out while this pair is finished
+        const int pn = p0 + pstep;
+        if (pn < p_end) pair_load(pr, kpool, vpool, btrow, pn, p_end, hkv, kvh, num_pages);
 
-    float lsum = 0.f;
-    float *s_p = s_buf;  // [CH][16 tokens][16 heads]
+        // mask keys past the sequence or on an absent page, then the pair's
+        // maximum per head
+        float mx = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < PPW; ++i) {
+        for (int j = 0; j < kPair; ++j)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const float p = __builtin_amdgcn_exp2f(s[i][r] - m);
-            lsum += p;
-            s_p[((wave + kWaves * i) * 16 + 4 * grp + r) * 16 + col] = p;
+            for (int i = 0; i < 4; ++i) {
+                const int tok = (p0 + j) * kPageSize + 4 * grp + i;
+                const float v = (ok[j] && tok < L) ? sc[j][i] * scale_log2 : -INFINITY;
+                sc[j][i] = v;
+                mx = fmaxf(mx, v);
+            }
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        if (__builtin_amdgcn_ballot_w64(mx > m_run + kRescaleLog2) != 0) {
+            const float m_new = fmaxf(m_run, mx);
+            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+            m_run = m_new;
+            l_run *= alpha;
+#pragma unroll
+            for (int db = 0; db < 8; ++db) oacc[db] *= alpha;
         }
-    }
-    lsum += __shfl_xor(lsum, 16);
-    lsum += __shfl_xor(lsum, 32);
-    __syncthreads();  // everyone is past reading s_red for m
-    if (grp == 0) s_red[wave][col] = lsum;
-    __syncthreads();
-    if (threadIdx.x < 16) {
-        s_ml[0][col] = m;
-        s_ml[1][col] = s_red[0][col] + s_red[1][col] + s_red[2][col] + s_red[3][col];
+        float p[kPair][4];
+#pragma unroll
+        for (int j = 0; j < kPair; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                p[j][i] = __builtin_amdgcn_exp2f(sc[j][i] - m_run);
+                l_run += p[j][i];
+            }
+        // P^T operand: k-slot e < 4 is token 4grp+e of page 0, e >= 4 token
+        // 16 + 4grp + e-4 of page 1 -- the V^T reads below use the same order
+        const uint4 pop = make_uint4(cvt2(p[0][0], p[0][1]), cvt2(p[0][2], p[0][3]),
+                                     cvt2(p[1][0], p[1][1]), cvt2(p[1][2], p[1][3]));
+#pragma unroll
+        for (int db = 0; db < 8; ++db) {
+            const i16x4 lo = lds_read_tr(vtr + 16 * db);
+            const i16x4 hi = lds_read_tr(vtr + 16 * VSTR + 16 * db);
+            const bf16x8 a = __builtin_bit_cast(
+                bf16x8, make_uint4(__builtin_bit_cast(uint2, lo).x, __builtin_bit_cast(uint2, lo).y,
+                                   __builtin_bit_cast(uint2, hi).x, __builtin_bit_cast(uint2, hi).y));
+            oacc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, pop), oacc[db], 0, 0, 0);
+        }
     }
 
-    // ---- o = sum_t p[t][h] * v[t][:] on the vector ALU
-    float acc[GP][8];
-#pragma unroll
-    for (int h = 0; h < GP; ++h)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
-#pragma unroll
-    for (int i = 0; i < PPW; ++i) {
-        if (!pin[i]) continue;
-#pragma unroll
-        for (int t4 = 0; t4 < 4; ++t4) {
-            const float *prow = s_p + ((wave + kWaves * i) * 16 + 4 * grp + t4) * 16;
-            float pw[GP];
-#pragma unroll
-            for (int h = 0; h < GP; ++h) pw[h] = prow[h];
-            const uint4 w = vr[i][t4];
-            const float v8[8] = {bf_lo(w.x), bf_hi(w.x), bf_lo(w.y), bf_hi(w.y),
-                                 bf_lo(w.z), bf_hi(w.z), bf_lo(w.w), bf_hi(w.w)};
-#pragma unroll
-            for (int h = 0; h < GP; ++h)
-#pragma unroll
-                for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pw[h], v8[e], acc[h][e]);
-        }
-    }
-#pragma unroll
-    for (int h = 0; h < GP; ++h)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            acc[h][e] += __shfl_xor(acc[h][e], 16);
-            acc[h][e] += __shfl_xor(acc[h][e], 32);
-        }
-    __syncthreads();  // s_p is dead; reuse the buffer for per-wave partial o
-    float *s_o = s_buf;  // [kWaves][GP][128]
+    // ---- merge the 4 waves: per-head (m, l) and O^T through LDS
+    l_run += __shfl_xor(l_run, 16);
+    l_run += __shfl_xor(l_run, 32);
     if (grp == 0) {
-#pragma unroll
-        for (int h = 0; h < GP; ++h)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) s_o[(wave * GP + h) * kHeadDim + 8 * col + e] = acc[h][e];
+        s_m[wave][col] = m_run;
+        s_l[wave][col] = l_run;
     }
+    __syncthreads();  // every wave is done with its V buffer: reuse it for O^T
+    float *s_o = reinterpret_cast<float *>(s_v);  // [kWaves][128 d][16 heads]
+#pragma unroll
+    for (int db = 0; db < 8; ++db)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) s_o[(wave * kHeadDim + 16 * db + 4 * grp + i) * 16 + col] = oacc[db][i];
     __syncthreads();
     for (int idx = threadIdx.x; idx < group * kHeadDim; idx += kThreads) {
         const int h = idx / kHeadDim, d = idx % kHeadDim;
-        float o = 0.f;
+        float M = -INFINITY;
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) o += s_o[(w * GP + h) * kHeadDim + d];
+        for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w][h]);
+        float lsum = 0.f, o = 0.f;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+            const float mw = s_m[w][h];
+            const float wt = mw == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mw - M);  // waves without pages
+            lsum += wt * s_l[w][h];
+            o += wt * s_o[(w * kHeadDim + d) * 16 + h];
+        }
         if (nch == 1) {
-            out[(static_cast<size_t>(b) * hq + kvh * group + h) * kHeadDim + d] = to_bf16(o / s_ml[1][h]);
+            out[(static_cast<size_t>(b) * hq + kvh * group + h) * kHeadDim + d] = to_bf16(o / lsum);
         } else {
             ws_o[(static_cast<size_t>(u) * group + h) * kHeadDim + d] = o;
-            if (d == 0) ws_ml[static_cast<size_t>(u) * group + h] = make_float2(s_ml[0][h], s_ml[1][h]);
+            if (d == 0) ws_ml[static_cast<size_t>(u) * group + h] = make_float2(M, lsum);
         }
     }
-    if (c == 0 && kvh == 0 && threadIdx.x == 0) ws_cbase[b] = s_loc[2];
+    if (c == 0 && kvh == 0 && threadIdx.x == 0) ws_cbase[b] = first;
 }
 
+// One work-group per (sequence, kv head); thread pairs (h, d).  The partials
+// of all chunks are loaded with independent loads (8 chunks in flight).
 __global__ void __launch_bounds__(kThreads)
 k_decode_combine(uint16_t *__restrict__ out, const int32_t *__restrict__ seq_lens,
                  const float *__restrict__ ws_o, const float2 *__restrict__ ws_ml,
@@ -268,18 +298,34 @@ k_decode_combine(uint16_t *__restrict__ out, const int32_t *__restrict__ seq_len
     for (int idx = threadIdx.x; idx < group * kHeadDim; idx += kThreads) {
         const int h = idx / kHeadDim, d = idx % kHeadDim;
         float M = -INFINITY;
-        for (int sidx = 0; sidx < nch; ++sidx) {
-            const float2 ml = ws_ml[(static_cast<size_t>(cbase + sidx) * hkv + kvh) * group + h];
-            if (ml.y > 0.f) M = fmaxf(M, ml.x);
+        for (int s0 = 0; s0 < nch; s0 += 8) {
+            float2 ml[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                ml[j] = s0 + j < nch ? ws_ml[(static_cast<size_t>(cbase + s0 + j) * hkv + kvh) * group + h]
+                                     : make_float2(-INFINITY, 0.f);
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (ml[j].y > 0.f) M = fmaxf(M, ml[j].x);
         }
         float lsum = 0.f, osum = 0.f;
-        for (int sidx = 0; sidx < nch; ++sidx) {
-            const size_t uu = (static_cast<size_t>(cbase + sidx) * hkv + kvh) * group + h;
-            const float2 ml = ws_ml[uu];
-            if (!(ml.y > 0.f)) continue;  // a chunk without keys contributes nothing
-            const float w = __builtin_amdgcn_exp2f(ml.x - M);
-            lsum += w * ml.y;
-            osum += w * ws_o[uu * kHeadDim + d];
+        for (int s0 = 0; s0 < nch; s0 += 8) {
+            float2 ml[8];
+            float o[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const size_t uu = (static_cast<size_t>(cbase + s0 + j) * hkv + kvh) * group + h;
+                const bool in = s0 + j < nch;
+                ml[j] = in ? ws_ml[uu] : make_float2(-INFINITY, 0.f);
+                o[j] = in ? ws_o[uu * kHeadDim + d] : 0.f;
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                if (!(ml[j].y > 0.f)) continue;  // a chunk without keys contributes nothing
+                const float w = __builtin_amdgcn_exp2f(ml[j].x - M);
+                lsum += w * ml[j].y;
+                osum += w * o[j];
+            }
         }
         out[(static_cast<size_t>(b) * hq + kvh * group + h) * kHeadDim + d] = to_bf16(osum / lsum);
     }
@@ -301,8 +347,8 @@ mw_status plan_decode(const mw_attn_shape *shape, int32_t batch, const int32_t *
         return fail(MW_ERR_INVALID_ARG, "%s: num_q_heads must be a positive multiple of num_kv_heads", who);
     if (shape->num_q_heads / shape->num_kv_heads > 16)
         return fail(MW_ERR_UNSUPPORTED, "%s: at most 16 query heads per kv head", who);
-    if (chunk_pages != 4 && chunk_pages != 8 && chunk_pages != 16)
-        return fail(MW_ERR_UNSUPPORTED, "%s: chunk_pages must be 4, 8 or 16 (or 0)", who);
+    if (chunk_pages < 8 || chunk_pages > 256 || chunk_pages % 8)
+        return fail(MW_ERR_UNSUPPORTED, "%s: chunk_pages must be a multiple of 8 in [8, 256] (or 0)", who);
     int64_t chunks = 0;
     for (int32_t b = 0; b < batch; ++b) {
         const int32_t L = h_seq_lens[b];
@@ -321,26 +367,14 @@ mw_status plan_decode(const mw_attn_shape *shape, int32_t batch, const int32_t *
     return MW_OK;
 }
 
-template <int GP, int PPW>
 void launch_split(dim3 grid, hipStream_t s, const mw_kv_pool *pool, const void *q, void *out,
                   const int32_t *seq_lens, const int32_t *bt, int bt_stride, char *ws, const Plan &pl,
-                  int batch, int hkv, int group, float scale_log2) {
-    hipLaunchKernelGGL((k_decode_split<GP, PPW>), grid, dim3(kThreads), 0, s, pool->k, pool->v,
+                  int batch, int hkv, int group, float scale_log2, int ch_pages) {
+    hipLaunchKernelGGL(k_decode_split, grid, dim3(kThreads), 0, s, pool->k, pool->v,
                        static_cast<const uint16_t *>(q), static_cast<uint16_t *>(out), seq_lens, bt,
                        bt_stride, reinterpret_cast<float *>(ws), reinterpret_cast<float2 *>(ws + pl.off_ml),
                        reinterpret_cast<int32_t *>(ws + pl.off_cbase), batch, hkv, group,
-                       pool->desc.num_pages, scale_log2);
-}
-
-template <int GP>
-void launch_split_g(int ppw, dim3 grid, hipStream_t s, const mw_kv_pool *pool, const void *q, void *out,
-                    const int32_t *seq_lens, const int32_t *bt, int bt_stride, char *ws, const Plan &pl,
-                    int batch, int hkv, int group, float scale_log2) {
-    switch (ppw) {
-        case 1: launch_split<GP, 1>(grid, s, pool, q, out, seq_lens, bt, bt_stride, ws, pl, batch, hkv, group, scale_log2); break;
-        case 2: launch_split<GP, 2>(grid, s, pool, q, out, seq_lens, bt, bt_stride, ws, pl, batch, hkv, group, scale_log2); break;
-        default: launch_split<GP, 4>(grid, s, pool, q, out, seq_lens, bt, bt_stride, ws, pl, batch, hkv, group, scale_log2); break;
-    }
+                       pool->desc.num_pages, scale_log2, ch_pages);
 }
 
 }  // namespace
@@ -351,7 +385,7 @@ mw_status mw_decode_workspace_size(const mw_attn_shape *shape, int32_t batch, co
                                    int32_t chunk_pages, size_t *bytes) {
     if (!bytes) return fail(MW_ERR_INVALID_ARG, "mw_decode_workspace_size: bytes is NULL");
     Plan pl;
-    mw_status st = plan_decode(shape, batch, h_seq_lens, chunk_pages ? chunk_pages : 16, 0, &pl,
+    mw_status st = plan_decode(shape, batch, h_seq_lens, chunk_pages ? chunk_pages : kDefaultChunkPages, 0, &pl,
                                "mw_decode_workspace_size");
     if (st != MW_OK) return st;
     *bytes = pl.bytes;
@@ -364,7 +398,7 @@ mw_status mw_decode_attn(const mw_kv_pool *pool, const mw_attn_shape *shape, int
                          size_t workspace_bytes, int32_t chunk_pages, mw_stream stream, mw_timing *timing) {
     const char *who = "mw_decode_attn";
     if (!pool || bt_stride < 1) return fail(MW_ERR_INVALID_ARG, "%s: bad pool or bt_stride", who);
-    if (chunk_pages == 0) chunk_pages = 16;
+    if (chunk_pages == 0) chunk_pages = kDefaultChunkPages;
     Plan pl;
     mw_status st = plan_decode(shape, batch, h_seq_lens, chunk_pages, bt_stride, &pl, who);
     if (st != MW_OK) return st;
@@ -389,17 +423,8 @@ mw_status mw_decode_attn(const mw_kv_pool *pool, const mw_attn_shape *shape, int
     char *ws = static_cast<char *>(d_workspace);
     if (pl.units > 0) {
         const dim3 grid(static_cast<unsigned>(pl.units));
-        const int ppw = chunk_pages / kWaves;
-        if (group <= 1)
-            launch_split_g<1>(ppw, grid, s, pool, d_q, d_out, d_seq_lens, d_block_table, bt_stride, ws, pl, batch, hkv, group, scale_log2);
-        else if (group <= 2)
-            launch_split_g<2>(ppw, grid, s, pool, d_q, d_out, d_seq_lens, d_block_table, bt_stride, ws, pl, batch, hkv, group, scale_log2);
-        else if (group <= 4)
-            launch_split_g<4>(ppw, grid, s, pool, d_q, d_out, d_seq_lens, d_block_table, bt_stride, ws, pl, batch, hkv, group, scale_log2);
-        else if (group <= 8)
-            launch_split_g<8>(ppw, grid, s, pool, d_q, d_out, d_seq_lens, d_block_table, bt_stride, ws, pl, batch, hkv, group, scale_log2);
-        else
-            launch_split_g<16>(ppw, grid, s, pool, d_q, d_out, d_seq_lens, d_block_table, bt_stride, ws, pl, batch, hkv, group, scale_log2);
+        launch_split(grid, s, pool, d_q, d_out, d_seq_lens, d_block_table, bt_stride, ws, pl, batch, hkv,
+                         group, scale_log2, chunk_pages);
         st = check_launch("k_decode_split");
         if (st != MW_OK) return st;
     }

@@ -88,7 +88,7 @@ def test_decode_workspace_size(lib):
     n = mw.mw_decode_workspace_size(8, 2, 128, [1, 256, 257], 16)
     units = 4 * 2
     assert n >= units * 4 * 128 * 4 + units * 4 * 8 + 3 * 4
-    assert mw.mw_decode_workspace_size(8, 2, 128, [1, 256, 257], 4) > n
+    assert mw.mw_decode_workspace_size(8, 2, 128, [1, 256, 257], 8) > n
     for args, status in [((8, 3, 128, [5]), mw.MW_ERR_INVALID_ARG),
                          ((8, 2, 64, [5]), mw.MW_ERR_UNSUPPORTED),
                          ((64, 2, 128, [5]), mw.MW_ERR_UNSUPPORTED),
@@ -96,9 +96,10 @@ def test_decode_workspace_size(lib):
         with pytest.raises(mw.MWError) as e:
             mw.mw_decode_workspace_size(*args)
         assert e.value.status == status
-    with pytest.raises(mw.MWError) as e:
-        mw.mw_decode_workspace_size(8, 2, 128, [5], 12)
-    assert e.value.status == mw.MW_ERR_UNSUPPORTED
+    for bad in (4, 12, 264):
+        with pytest.raises(mw.MWError) as e:
+            mw.mw_decode_workspace_size(8, 2, 128, [5], bad)
+        assert e.value.status == mw.MW_ERR_UNSUPPORTED
 
 
 def test_attention_calls_reject_bad_arguments_before_launching(lib):

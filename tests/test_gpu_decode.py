@@ -10,8 +10,9 @@ from tests.helpers import assert_close, say
 
 pytestmark = pytest.mark.gpu
 
-# lengths on and around page and chunk boundaries (16-token pages, 4..16-page chunks)
-EDGE_LENS = [1, 2, 15, 16, 17, 63, 64, 65, 255, 256, 257, 1000, 1023, 1024, 1025, 4097]
+# lengths on and around page and chunk boundaries (16-token pages, 32-page chunks)
+EDGE_LENS = [1, 2, 15, 16, 17, 31, 32, 33, 63, 64, 65, 255, 256, 257, 511, 512, 513, 1000,
+             1023, 1024, 1025, 4097]
 
 
 def run_decode(wl, chunk_pages=0, q_scale=None):
@@ -36,7 +37,7 @@ def test_decode_matches_oracle_on_edge_lengths(hq, hkv, q_scale):
     assert_close(got, ref, f"decode hq={hq} hkv={hkv}")
 
 
-@pytest.mark.parametrize("chunk_pages", [4, 8, 16])
+@pytest.mark.parametrize("chunk_pages", [8, 16, 32, 64])
 def test_decode_split_count_invariance(chunk_pages):
     say(f"decode chunk_pages={chunk_pages}")
     cfg = W.custom_config(hq=32, hkv=8, pre_chunks=((0, 1),), dec_batch=12, dec_len_lo=1,
