@@ -60,6 +60,9 @@ def parse():
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-parity", action="store_true")
     ap.add_argument("--table", default="", help="also write the per-partition table (Markdown) here")
+    ap.add_argument("--traffic-pass", action="store_true",
+                    help="run each kernel once on its partition plus a device copy of known size "
+                         "(the command profiled by rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE), then exit")
     return ap.parse_args()
 
 
@@ -115,28 +118,42 @@ class Bench:
         """Per-call latency of one phase alone on `stream`: kernel ms lists."""
         torch = self.torch
         outs = {"call": [], "k0": [], "k1": [], "append": []}
-        tws = [self.Timing() for _ in range(reps)]
-        tks = [[self.Timing() for _ in self.chunks] if which == "prefill" else self.Timing()
-               for _ in range(reps)]
+        nchunk = len(self.chunks) if which == "prefill" else 1
+        tws = [[self.Timing() for _ in range(nchunk)] for _ in range(reps)]
+        tks = [[self.Timing() for _ in range(nchunk)] for _ in range(reps)]
         torch.cuda.synchronize()
         for i in range(reps):
             if which == "prefill":
-                for (r, n), (k, v), tk in zip(self.chunks, self.pre_new, tks[i]):
-                    self.dw.write_prefill_kv(r, n, k, v, stream, tws[i].h)
+                for (r, n), (k, v), tw, tk in zip(self.chunks, self.pre_new, tws[i], tks[i]):
+                    self.dw.write_prefill_kv(r, n, k, v, stream, tw.h)
                     self.dw.prefill(r, n, stream, tk.h)
             else:
-                self.decode_call(stream, tws[i], tks[i])
+                self.decode_call(stream, tws[i][0], tks[i][0])
         torch.cuda.synchronize()
         for i in range(reps):
-            if which == "prefill":
-                outs["k0"].append(sum(tk.kernel_ms(0) for tk in tks[i]))
-                outs["call"].append(sum(tk.elapsed()[0] for tk in tks[i]))
-            else:
-                outs["k0"].append(tks[i].kernel_ms(0))
-                outs["k1"].append(tks[i].kernel_ms(1))
-                outs["call"].append(tks[i].elapsed()[0])
-            outs["append"].append(tws[i].elapsed()[0])
+            outs["k0"].append(sum(tk.kernel_ms(0) for tk in tks[i]))
+            outs["call"].append(sum(tk.elapsed()[0] for tk in tks[i]))
+            if which == "decode":
+                outs["k1"].append(tks[i][0].kernel_ms(1))
+            outs["append"].append(sum(tw.elapsed()[0] for tw in tws[i]))
         return outs
+
+    def stream_ceiling(self, stream, n_cus, nbytes=1 << 30, reps=5):
+        """HBM read rate the CUs of `stream` reach on a plain 1 GiB stream."""
+        from paper_2504_14489_amd import mw
+        torch = self.torch
+        if not hasattr(self, "_stream_buf"):
+            self._stream_buf = torch.empty(nbytes, dtype=torch.uint8, device=self.dw.device)
+            self._sink = torch.empty(1 << 16, dtype=torch.int32, device=self.dw.device)
+        blocks = 8 * n_cus
+        ts = [self.Timing() for _ in range(reps + 1)]
+        torch.cuda.synchronize()
+        for t in ts:
+            mw.mw_stream_read(self._stream_buf.data_ptr(), nbytes, self._sink.data_ptr(), blocks,
+                              stream, t.h)
+        torch.cuda.synchronize()
+        ms = median([t.kernel_ms(0) for t in ts[1:]])
+        return nbytes / (ms * 1e-3) / 1e9
 
     # ------------------------------------------------------- multiplexed --
     def multiplexed(self, part, steps, m):
@@ -168,6 +185,58 @@ class Bench:
 
     def close(self):
         self.dw.close()
+
+
+KERNEL_SOURCES = {"k_prefill_attn": "prefill_attn.hip", "k_decode_split": "decode_attn.hip"}
+
+
+def source_sha(kernel):
+    import hashlib
+    path = os.path.join(ROOT, "paper_2504_14489_amd", "csrc", KERNEL_SOURCES[kernel])
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def committed_traffic(kernel, workload):
+    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
+    summary, scaled by the copy-kernel calibration it records; None when the
+    summary is missing or the kernel's source has changed since."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get(f"{kernel}.source_sha256_16") != source_sha(kernel):
+        return None
+    try:
+        return float(vals[f"{kernel}.traffic_bytes"])
+    except (KeyError, ValueError):
+        return None
+
+
+def traffic_pass(args):
+    """One isolated launch of each kernel on its partition, then a device copy
+    of known size for the counter calibration."""
+    import torch
+    b = Bench(args)
+    p_cus, d_cus = b.cfg.prefill_cus[0], b.cfg.decode_cus[0]
+    part = b.Partition(p_cus, d_cus)
+    try:
+        b.prefill_call(part.prefill_stream)
+        torch.cuda.synchronize()
+        b.decode_call(part.decode_stream)
+        torch.cuda.synchronize()
+        src = torch.empty(256 << 20, dtype=torch.uint8, device=b.dw.device)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+    finally:
+        part.close()
+        b.close()
+    log(f"[bench] traffic pass done: {b.cfg.name}, copy of {256 << 20} bytes")
 
 
 def cpu_baseline(wl, cfg, seconds):
@@ -258,6 +327,7 @@ def run_partition(b, p_cus, d_cus, args):
         iso_d = b.isolated("decode", ds, reps)
         solo_p = b.isolated("prefill", b.full.cuda_stream, reps)
         solo_d = b.isolated("decode", b.full.cuda_stream, reps)
+        ceiling = b.stream_ceiling(ds, d_cus)
         # isolated outputs, for the bit-exact comparison with multiplexed ones
         b.prefill_call(ps)
         b.decode_call(ds)
@@ -293,6 +363,7 @@ def run_partition(b, p_cus, d_cus, args):
             "prefill_window_ms": mux["prefill_window_ms"], "decode_window_ms": mux["decode_window_ms"],
         },
         "mux_equals_isolated_bitwise": same,
+        "decode_partition_stream_read_gbs": ceiling,
     }
     res["slowdown"] = {
         "prefill": res["mux"]["prefill_kernel_ms"] / res["iso"]["prefill_kernel_ms"],
@@ -319,8 +390,10 @@ def roofline_entries(b, res):
     dec["frac"] = dec["achieved"] / dec["peak"]
     dec["share_peak"] = HBM_PEAK_GBS * res["decode_cus"] / N_CU
     dec["frac_share"] = dec["achieved"] / dec["share_peak"]
+    dec["measured_ceiling"] = res["decode_partition_stream_read_gbs"]
+    dec["frac_measured"] = dec["achieved"] / dec["measured_ceiling"]
     for e in (pre, dec):
-        e["traffic"] = None
+        e["traffic"] = committed_traffic(e["kernel"], b.cfg.name)
     # dominant = larger share of the step's GPU time
     pre_total = pre_ms
     dec_total = dec_ms * res["decode_iters_per_step"]
@@ -337,6 +410,9 @@ def main():
     if not torch.cuda.is_available():
         log("bench.py needs a GPU")
         sys.exit(1)
+    if args.traffic_pass:
+        traffic_pass(args)
+        return
     b = Bench(args)
     cfg = b.cfg
     splits = list(zip(cfg.prefill_cus, cfg.decode_cus))

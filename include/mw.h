@@ -68,6 +68,7 @@ typedef int32_t mw_status;
 #define MW_ERR_NOT_READY (-5)    /* a timing was read before it was recorded    */
 
 typedef void *mw_stream; /* a hipStream_t */
+typedef struct mw_timing mw_timing; /* per-call GPU timing events (see below) */
 
 /* Text of the calling thread's last error ("" if none).  The pointer stays
  * valid until the thread's next failing call. */
@@ -121,7 +122,6 @@ mw_status mw_kv_pool_num_free(const mw_kv_pool *pool, int32_t *n_free);
  *   d_start_pos device[batch]   same values as h_start_pos
  *   d_block_table device [batch][bt_stride]
  * `timing` may be NULL. */
-typedef struct mw_timing mw_timing;
 mw_status mw_kv_pool_write(const mw_kv_pool *pool, int32_t batch, const int32_t *h_new_lens,
                            const int32_t *h_start_pos, const int32_t *d_qo_indptr,
                            const int32_t *d_start_pos, const int32_t *d_block_table,
@@ -169,6 +169,14 @@ mw_status mw_partition_destroy(mw_partition *part);
  * shader clocks (low 32 bits of the 100 MHz real-time counter). */
 mw_status mw_cu_probe(int32_t n_blocks, int32_t spin_cycles, uint32_t *d_out,
                       mw_stream stream);
+
+/* Measured HBM read ceiling: reads `bytes` (a multiple of 16, 16-byte aligned)
+ * from d_src once with n_blocks 256-thread work-groups on `stream` (so on that
+ * stream's CUs) and writes one word per work-group to d_sink[n_blocks].  Used
+ * to report attention bandwidth against what the same CUs can stream.
+ * `timing` may be NULL. */
+mw_status mw_stream_read(const void *d_src, size_t bytes, uint32_t *d_sink, int32_t n_blocks,
+                         mw_stream stream, mw_timing *timing);
 
 /* ------------------------------------------------------------------------
  * Per-call timing.  A call given a timing handle records a start event, one

@@ -276,3 +276,49 @@ extern "C" mw_status mw_cu_probe(int32_t n_blocks, int32_t spin_cycles, uint32_t
                        d_out, spin_cycles);
     return check_launch("k_cu_probe");
 }
+
+// ------------------------------------------------------- stream read ------
+// Reads `bytes` (a multiple of 16) once with 16-byte loads, grid-stride, 8
+// loads in flight per thread; each block folds what it read into one word of
+// d_sink[block] so the loads cannot be dropped.
+__global__ void __launch_bounds__(256) k_stream_read(const uint4 *__restrict__ src, size_t n_vec,
+                                                     uint32_t *__restrict__ sink) {
+    const size_t stride = static_cast<size_t>(gridDim.x) * blockDim.x;
+    size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    uint32_t acc = 0;
+    for (; i + 7 * stride < n_vec; i += 8 * stride) {
+        uint4 v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = src[i + j * stride];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc ^= v[j].x ^ v[j].y ^ v[j].z ^ v[j].w;
+    }
+    for (; i < n_vec; i += stride) {
+        const uint4 v = src[i];
+        acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
+    __shared__ uint32_t red[256];
+    red[threadIdx.x] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t a = 0;
+        for (int t = 0; t < 256; ++t) a ^= red[t];
+        sink[blockIdx.x] = a;
+    }
+}
+
+extern "C" mw_status mw_stream_read(const void *d_src, size_t bytes, uint32_t *d_sink, int32_t n_blocks,
+                                    mw_stream stream, mw_timing *timing) {
+    if (!d_src || !d_sink || bytes % 16 || !aligned16(d_src) || n_blocks < 1 || n_blocks > (1 << 20))
+        return fail(MW_ERR_INVALID_ARG, "mw_stream_read: bad arguments");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    mw_status st = timing_begin(timing, s);
+    if (st != MW_OK) return st;
+    hipLaunchKernelGGL(k_stream_read, dim3(n_blocks), dim3(256), 0, s, static_cast<const uint4 *>(d_src),
+                       bytes / 16, d_sink);
+    st = check_launch("k_stream_read");
+    if (st != MW_OK) return st;
+    st = timing_kernel_done(timing, s);
+    timing_end(timing);
+    return st;
+}
