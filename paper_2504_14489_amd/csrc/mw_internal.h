@@ -21,6 +21,10 @@ mw_status fail(mw_status st, const char *fmt, ...) __attribute__((format(printf,
 
 inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// Number of CUs a stream's kernels may run on (its CU mask; all CUs of the
+// current device for a stream without one).
+int stream_cus(hipStream_t s);
+
 }  // namespace mw
 
 #define MW_HIP_TRY(expr)                                                                  \

@@ -114,14 +114,15 @@ k_prefill_attn(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ 
                const uint16_t *__restrict__ q, uint16_t *__restrict__ out,
                const int32_t *__restrict__ qo_indptr, const int32_t *__restrict__ prefix_lens,
                const int32_t *__restrict__ bt, int bt_stride, int hkv, int group, int num_pages,
-               float scale_log2, int max_pairs, int n_hgroups) {
+               float scale_log2, int paired, int n_hgroups) {
     __shared__ __attribute__((aligned(1024))) uint16_t s_k[2 * TILE];
     __shared__ __attribute__((aligned(1024))) uint16_t s_v[2 * TILE];
     __shared__ int32_t s_bt[kBtCache];
 
-    // Work-group = one pair of query blocks of one (sequence, kv head, head
-    // group): block nqb-1-i and block i.  Causal blocks grow linearly with the
-    // block index, so every pair costs about the same number of key tiles.
+    // Work-group = one query block of one (sequence, kv head, head group),
+    // heaviest blocks first, or (paired) the pair of blocks nqb-1-i and i:
+    // causal blocks grow linearly with the block index, so every pair costs
+    // about the same number of key tiles.
     const int b = blockIdx.y;
     const int x = blockIdx.x;
     const int kvh = x % hkv;
@@ -130,8 +131,8 @@ k_prefill_attn(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ 
     const int row0 = qo_indptr[b];
     const int n = qo_indptr[b + 1] - row0;
     const int nqb = (n + BM - 1) / BM;
-    if (pair >= (nqb + 1) / 2) return;
-    const int n_items = (pair == nqb - 1 - pair) ? 1 : 2;
+    if (pair >= (paired ? (nqb + 1) / 2 : nqb)) return;
+    const int n_items = (!paired || pair == nqb - 1 - pair) ? 1 : 2;
     const int r = prefix_lens[b];
     const int32_t *btrow = bt + static_cast<size_t>(b) * bt_stride;
     const int np_seq = min((r + n + kPageSize - 1) / kPageSize, bt_stride);
@@ -463,14 +464,24 @@ extern "C" mw_status mw_prefill_attn(const mw_kv_pool *pool, const mw_attn_shape
         const int hkv = shape->num_kv_heads;
         const int group = shape->num_q_heads / hkv;
         const int n_hgroups = (group + 3) / 4;
-        const int64_t max_pairs = ((max_n + BM - 1) / BM + 1) / 2;
-        const int64_t gx = max_pairs * hkv * n_hgroups;
+        const int64_t max_qblocks = (max_n + BM - 1) / BM;
+        // Pair blocks only when the pairs fill whole rounds of the CUs the
+        // stream may use (one work-group fits per CU): equal-cost pairs then
+        // finish together.  Otherwise single blocks, heaviest first, fill the
+        // last round better.
+        int64_t n_pairs = 0;
+        for (int32_t b = 0; b < batch; ++b) n_pairs += ((h_new_lens[b] + BM - 1) / BM + 1) / 2;
+        n_pairs *= hkv * n_hgroups;
+        const int64_t cus = stream_cus(s);
+        const int64_t rounds = (n_pairs + cus - 1) / cus;
+        const int paired = n_pairs >= cus && rounds * cus * 20 <= n_pairs * 21;
+        const int64_t gx = (paired ? (max_qblocks + 1) / 2 : max_qblocks) * hkv * n_hgroups;
         if (gx > 0x7fffffff) return fail(MW_ERR_UNSUPPORTED, "%s: grid too large", who);
         auto kernel = max_pages <= kBtCache ? k_prefill_attn<true> : k_prefill_attn<false>;
         hipLaunchKernelGGL(kernel, dim3(static_cast<unsigned>(gx), batch), dim3(kThreads), 0, s, pool->k,
                            pool->v, static_cast<const uint16_t *>(d_q), static_cast<uint16_t *>(d_out), d_qo_indptr,
                            d_prefix_lens, d_block_table, bt_stride, hkv, group, pool->desc.num_pages,
-                           shape->scale * kLog2e, static_cast<int>(max_pairs), n_hgroups);
+                           shape->scale * kLog2e, paired, n_hgroups);
         st = check_launch("k_prefill_attn");
         if (st != MW_OK) return st;
     }

@@ -19,6 +19,21 @@ mw_status fail(mw_status st, const char *fmt, ...) {
     return st;
 }
 
+int stream_cus(hipStream_t s) {
+    uint32_t mask[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    int n = 0;
+    if (hipExtStreamGetCUMask(s, 8, mask) == hipSuccess)
+        for (uint32_t m : mask) n += __builtin_popcount(m);
+    if (n > 0) return n;
+    (void)hipGetLastError();  // a failed query is not an error of the caller's work
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0)
+        return cus;
+    (void)hipGetLastError();
+    return 256;
+}
+
 mw_status check_launch(const char *what) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(MW_ERR_HIP, "launch of %s failed: %s", what, hipGetErrorString(e));

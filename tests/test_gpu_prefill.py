@@ -119,3 +119,31 @@ def test_prefill_varlen_batch():
         ref = oracle.prefill(w.q_pre[r:r + n], w.k_pool, w.v_pool, w.pre_bt, r)
         assert_close(got[row:row + n], ref, f"varlen seq r={r} n={n}")
         row += n
+
+
+def test_prefill_same_result_on_any_cu_count():
+    """The launch pairs heavy and light query blocks only when the pairs fill
+    whole rounds of the stream's CUs; either split must give the same bits."""
+    say("prefill split independence (32 / 64 / all CUs)")
+    from paper_2504_14489_amd.device import Partition
+    cfg = W.custom_config(hq=32, hkv=8, pre_chunks=((0, 512),), dec_batch=1, dec_len_lo=1,
+                          dec_len_hi=2, seed=21)
+    wl = W.make_workload(cfg)
+    dw = DeviceWorkload(wl)
+    outs = []
+    try:
+        for p_cus in (32, 64, 0):  # 32 pairs: paired on 32 CUs, single blocks otherwise
+            part = Partition(p_cus, 256 - p_cus) if p_cus else None
+            try:
+                o = dw.prefill(0, 512, part.prefill_stream if part else 0)
+                torch.cuda.synchronize()
+                outs.append(to_bits(o))
+            finally:
+                if part:
+                    part.close()
+    finally:
+        dw.close()
+    assert np.array_equal(outs[0], outs[1]) and np.array_equal(outs[0], outs[2]), "split changed the result"
+    rows = [0, 63, 64, 255, 511]
+    ref = oracle.prefill(wl.q_pre[:512], wl.k_pool, wl.v_pool, wl.pre_bt, 0)
+    assert_close(outs[0][rows], ref[rows], "split independence rows")
