@@ -250,6 +250,73 @@ mw_status mw_decode_attn(const mw_kv_pool *pool, const mw_attn_shape *shape, int
                          void *d_out, void *d_workspace, size_t workspace_bytes,
                          int32_t chunk_pages, mw_stream stream, mw_timing *timing);
 
+/* ------------------------------------------------------------------------ *
+ * Contention-tolerant estimator (paper Sec. 3.3) and the prefill-layer count
+ * of the dispatcher (Sec. 3.4).  Host-side only: these calls touch no GPU.
+ * ------------------------------------------------------------------------ */
+
+/* Solo-run predictor (Sec. 3.3, "Solo-run predictor", Eqs. (1) and (2)):
+ * per-call latency models fitted to measured solo runs, one model per phase
+ * and per partition size (number of CUs the phase runs on):
+ *     T_prefill = th1 * sum_i n_i^2 + th2 * sum_i n_i r_i + th3 * sum_i n_i + th4
+ *     T_decode  = th1 * sum_i r_i + th2 * bs + th3
+ * with n_i the new and r_i the reused (cached) tokens of sequence i; a decode
+ * sequence of context length L has r = L - 1 (its own token is the new one).
+ * The fit minimises the squared relative error (each sample's equation is
+ * divided by its measured time), which is what the paper's accuracy figure
+ * (maximum relative deviation) measures.  Times are in milliseconds.
+ *
+ *   mw_predictor_add_*: record one measured call.  Lengths are host arrays of
+ *       `batch` entries (n >= 1, r >= 0; L >= 1); ms > 0 and finite.
+ *   mw_predictor_fit: fits every (phase, cus) with at least as many samples
+ *       as coefficients; MW_ERR_NOT_READY if none has.
+ *   mw_predictor_*_ms: the model's prediction; MW_ERR_NOT_READY if no model
+ *       was fitted for that phase and partition size.
+ *   mw_predictor_coefficients: th1..th4 (prefill) or th1..th3 (decode, th[3]
+ *       set to 0) of a fitted model.  phase: 0 = prefill, 1 = decode. */
+typedef struct mw_predictor mw_predictor;
+mw_status mw_predictor_create(mw_predictor **out);
+mw_status mw_predictor_destroy(mw_predictor *p);
+mw_status mw_predictor_add_prefill(mw_predictor *p, int32_t cus, int32_t batch, const int32_t *new_lens,
+                                   const int32_t *prefix_lens, double ms);
+mw_status mw_predictor_add_decode(mw_predictor *p, int32_t cus, int32_t batch, const int32_t *seq_lens,
+                                  double ms);
+mw_status mw_predictor_fit(mw_predictor *p);
+mw_status mw_predictor_prefill_ms(const mw_predictor *p, int32_t cus, int32_t batch, const int32_t *new_lens,
+                                  const int32_t *prefix_lens, double *ms);
+mw_status mw_predictor_decode_ms(const mw_predictor *p, int32_t cus, int32_t batch, const int32_t *seq_lens,
+                                 double *ms);
+mw_status mw_predictor_coefficients(const mw_predictor *p, int32_t phase, int32_t cus, double theta[4]);
+
+/* Contention guard (Sec. 3.3, "Contention guard"): the maximum decode
+ * slowdown (multiplexed / solo latency) seen in each cell of a grid over five
+ * variables: prefill new tokens, prefill reused tokens, decode batch size,
+ * decode reused tokens in total, and the prefill partition size.  Token
+ * counts fall into powers-of-4 cells (x in (4^(k-1), 4^k] is cell k; 0 and 1
+ * are cell 0), batch sizes into powers-of-2 cells, the partition size is
+ * matched exactly.  Samples raise a cell's maximum, so the guard can keep
+ * learning from run-time measurements.
+ *   mw_guard_add: slowdown > 0 and finite; counts >= 0, batch >= 1, cus >= 1.
+ *   mw_guard_lookup: the cell's maximum; for a cell without samples the
+ *       maximum over all cells of the same partition size, then over all
+ *       cells; 1.0 for an empty guard.
+ * Worst-case decode latency = predicted solo latency x guard slowdown. */
+typedef struct {
+    int64_t prefill_new, prefill_reused, decode_batch, decode_reused;
+    int32_t prefill_cus;
+} mw_guard_key;
+typedef struct mw_guard mw_guard;
+mw_status mw_guard_create(mw_guard **out);
+mw_status mw_guard_destroy(mw_guard *g);
+mw_status mw_guard_add(mw_guard *g, const mw_guard_key *key, double slowdown);
+mw_status mw_guard_lookup(const mw_guard *g, const mw_guard_key *key, double *slowdown);
+
+/* Number of prefill layers to launch next to one decode iteration (Sec. 3.4):
+ * N_PL = ceil(T_d * N_T / T_P) with T_d the estimated decode latency, T_P the
+ * estimated latency of the whole prefill and N_T the model's layer count;
+ * the result is clamped to [1, N_T].  Times > 0 and finite, n_layers >= 1. */
+mw_status mw_prefill_layers(double t_decode_ms, double t_prefill_ms, int32_t n_layers, int32_t *n_pl);
+
 #ifdef __cplusplus
 }
 #endif

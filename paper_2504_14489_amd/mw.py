@@ -41,6 +41,13 @@ class _PoolDesc(ctypes.Structure):
                 ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32)]
 
 
+class GuardKey(ctypes.Structure):
+    """mw_guard_key: the five variables of a contention-guard cell."""
+    _fields_ = [("prefill_new", ctypes.c_int64), ("prefill_reused", ctypes.c_int64),
+                ("decode_batch", ctypes.c_int64), ("decode_reused", ctypes.c_int64),
+                ("prefill_cus", ctypes.c_int32)]
+
+
 class _AttnShape(ctypes.Structure):
     _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("scale", ctypes.c_float)]
@@ -52,6 +59,7 @@ _I = ctypes.c_int32
 _PI = ctypes.POINTER(ctypes.c_int32)
 _PU = ctypes.POINTER(ctypes.c_uint32)
 _PF = ctypes.POINTER(ctypes.c_float)
+_PD = ctypes.POINTER(ctypes.c_double)
 
 _SIGNATURES = {
     "mw_last_error": ([], ctypes.c_char_p),
@@ -85,6 +93,19 @@ _SIGNATURES = {
                                   ctypes.POINTER(ctypes.c_size_t)], _I),
     "mw_decode_attn": ([_P, ctypes.POINTER(_AttnShape), _I, _PI, _P, _P, _I, _P, _P, _P,
                         ctypes.c_size_t, _I, _P, _P], _I),
+    "mw_predictor_create": ([ctypes.POINTER(_P)], _I),
+    "mw_predictor_destroy": ([_P], _I),
+    "mw_predictor_add_prefill": ([_P, _I, _I, _PI, _PI, ctypes.c_double], _I),
+    "mw_predictor_add_decode": ([_P, _I, _I, _PI, ctypes.c_double], _I),
+    "mw_predictor_fit": ([_P], _I),
+    "mw_predictor_prefill_ms": ([_P, _I, _I, _PI, _PI, _PD], _I),
+    "mw_predictor_decode_ms": ([_P, _I, _I, _PI, _PD], _I),
+    "mw_predictor_coefficients": ([_P, _I, _I, _PD], _I),
+    "mw_guard_create": ([ctypes.POINTER(_P)], _I),
+    "mw_guard_destroy": ([_P], _I),
+    "mw_guard_add": ([_P, ctypes.POINTER(GuardKey), ctypes.c_double], _I),
+    "mw_guard_lookup": ([_P, ctypes.POINTER(GuardKey), _PD], _I),
+    "mw_prefill_layers": ([ctypes.c_double, ctypes.c_double, _I, _PI], _I),
 }
 
 EXPORTED = tuple(_SIGNATURES)
@@ -307,3 +328,83 @@ def mw_decode_attn(pool, num_q_heads: int, num_kv_heads: int, head_dim: int, sca
     _check(load().mw_decode_attn(pool, ctypes.byref(sh), len(sl), _pi(sl), _h(d_seq_lens),
                                  _h(d_block_table), bt_stride, _h(d_q), _h(d_out), _h(d_workspace),
                                  workspace_bytes, chunk_pages, _h(stream), timing))
+
+
+# ---- contention-tolerant estimator (host-side)
+
+def mw_predictor_create():
+    p = _P()
+    _check(load().mw_predictor_create(ctypes.byref(p)))
+    return p
+
+
+def mw_predictor_destroy(p):
+    _check(load().mw_predictor_destroy(p))
+
+
+def mw_predictor_add_prefill(p, cus: int, new_lens, prefix_lens, ms: float):
+    n, r = _i32(new_lens), _i32(prefix_lens)
+    if len(n) != len(r):
+        raise ValueError("new_lens and prefix_lens differ in length")
+    _check(load().mw_predictor_add_prefill(p, cus, len(n), _pi(n), _pi(r), ms))
+
+
+def mw_predictor_add_decode(p, cus: int, seq_lens, ms: float):
+    lens = _i32(seq_lens)
+    _check(load().mw_predictor_add_decode(p, cus, len(lens), _pi(lens), ms))
+
+
+def mw_predictor_fit(p):
+    _check(load().mw_predictor_fit(p))
+
+
+def mw_predictor_prefill_ms(p, cus: int, new_lens, prefix_lens) -> float:
+    n, r = _i32(new_lens), _i32(prefix_lens)
+    if len(n) != len(r):
+        raise ValueError("new_lens and prefix_lens differ in length")
+    out = ctypes.c_double()
+    _check(load().mw_predictor_prefill_ms(p, cus, len(n), _pi(n), _pi(r), ctypes.byref(out)))
+    return out.value
+
+
+def mw_predictor_decode_ms(p, cus: int, seq_lens) -> float:
+    lens = _i32(seq_lens)
+    out = ctypes.c_double()
+    _check(load().mw_predictor_decode_ms(p, cus, len(lens), _pi(lens), ctypes.byref(out)))
+    return out.value
+
+
+def mw_predictor_coefficients(p, phase: int, cus: int) -> np.ndarray:
+    th = (ctypes.c_double * 4)()
+    _check(load().mw_predictor_coefficients(p, phase, cus, th))
+    return np.array(th[:], dtype=np.float64)
+
+
+def mw_guard_create():
+    g = _P()
+    _check(load().mw_guard_create(ctypes.byref(g)))
+    return g
+
+
+def mw_guard_destroy(g):
+    _check(load().mw_guard_destroy(g))
+
+
+def mw_guard_add(g, prefill_new: int, prefill_reused: int, decode_batch: int, decode_reused: int,
+                 prefill_cus: int, slowdown: float):
+    key = GuardKey(prefill_new, prefill_reused, decode_batch, decode_reused, prefill_cus)
+    _check(load().mw_guard_add(g, ctypes.byref(key), slowdown))
+
+
+def mw_guard_lookup(g, prefill_new: int, prefill_reused: int, decode_batch: int, decode_reused: int,
+                    prefill_cus: int) -> float:
+    key = GuardKey(prefill_new, prefill_reused, decode_batch, decode_reused, prefill_cus)
+    out = ctypes.c_double()
+    _check(load().mw_guard_lookup(g, ctypes.byref(key), ctypes.byref(out)))
+    return out.value
+
+
+def mw_prefill_layers(t_decode_ms: float, t_prefill_ms: float, n_layers: int) -> int:
+    out = ctypes.c_int32()
+    _check(load().mw_prefill_layers(t_decode_ms, t_prefill_ms, n_layers, ctypes.byref(out)))
+    return out.value

@@ -1,0 +1,289 @@
+"""Offline profiling for the contention-tolerant estimator (paper Sec. 3.3).
+
+Measures, on CU partitions of one GPU, the solo-run latency of prefill and
+decode attention calls and the decode slowdown when a prefill call runs next
+to it, then fits the solo-run predictor (Eqs. (1)-(2)) and fills the
+contention guard through the C ABI.  Lengths follow a grid at powers of 4, as
+the paper samples its 5 variables, scaled to what one GPU profiles in a few
+minutes; held-out random samples measure the predictor's accuracy.
+
+    python -m paper_2504_14489_amd.profiling --out results.json
+
+K/V pools and queries are random bf16 generated on the device: latency does
+not depend on the values.  Every call runs in the library's kernels.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import statistics
+import sys
+import time
+
+import numpy as np
+import torch
+
+from . import mw
+from .device import Partition, Timing
+
+HQ, HKV, D, PAGE = 32, 8, 128, 16
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class Pool:
+    """A random paged K/V pool and the buffers of one model shape."""
+
+    def __init__(self, num_pages: int, seed: int = 0, device: str = "cuda:0"):
+        self.dev = torch.device(device)
+        g = torch.Generator(device=self.dev).manual_seed(seed)
+        shape = (num_pages, HKV, PAGE, D)
+        self.k = torch.randn(shape, generator=g, device=self.dev, dtype=torch.bfloat16)
+        self.v = torch.randn(shape, generator=g, device=self.dev, dtype=torch.bfloat16)
+        self.num_pages = num_pages
+        self.pool = mw.mw_kv_pool_create(num_pages, PAGE, HKV, D, self.k.data_ptr(), self.v.data_ptr())
+        self.perm = np.random.default_rng(seed).permutation(num_pages).astype(np.int32)
+        self.scale = 1.0 / math.sqrt(D)
+        self.gen = g
+
+    def close(self):
+        mw.mw_kv_pool_destroy(self.pool)
+
+    def tables(self, lens):
+        """Block-table rows for sequences of the given lengths (distinct pages)."""
+        pages = [(int(L) + PAGE - 1) // PAGE for L in lens]
+        stride = max(pages)
+        if sum(pages) > self.num_pages:
+            raise ValueError("pool too small for this sample")
+        bt = np.zeros((len(lens), stride), np.int32)
+        off = 0
+        for i, p in enumerate(pages):
+            bt[i, :p] = self.perm[off:off + p]
+            off += p
+        return torch.from_numpy(bt).to(self.dev), stride
+
+    def rand(self, *shape):
+        return torch.randn(shape, generator=self.gen, device=self.dev, dtype=torch.bfloat16)
+
+
+class PrefillCall:
+    def __init__(self, pool: Pool, n: int, r: int):
+        self.p, self.n, self.r = pool, n, r
+        self.bt, self.stride = pool.tables([r + n])
+        self.q = pool.rand(n, HQ, D)
+        self.o = torch.empty_like(self.q)
+        self.indptr = torch.tensor([0, n], dtype=torch.int32, device=pool.dev)
+        self.pref = torch.tensor([r], dtype=torch.int32, device=pool.dev)
+
+    def __call__(self, stream, timing=None):
+        mw.mw_prefill_attn(self.p.pool, HQ, HKV, D, self.p.scale, [self.n], [self.r], self.indptr.data_ptr(),
+                           self.pref.data_ptr(), self.bt.data_ptr(), self.stride, self.q.data_ptr(),
+                           self.o.data_ptr(), stream, timing)
+
+
+class DecodeCall:
+    def __init__(self, pool: Pool, lens):
+        self.p = pool
+        self.lens = np.asarray(lens, np.int32)
+        self.bt, self.stride = pool.tables(self.lens)
+        self.d_lens = torch.from_numpy(self.lens).to(pool.dev)
+        self.q = pool.rand(len(self.lens), HQ, D)
+        self.o = torch.empty_like(self.q)
+        nbytes = mw.mw_decode_workspace_size(HQ, HKV, D, self.lens, 0)
+        self.ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=pool.dev)
+
+    def __call__(self, stream, timing=None):
+        mw.mw_decode_attn(self.p.pool, HQ, HKV, D, self.p.scale, self.lens, self.d_lens.data_ptr(),
+                          self.bt.data_ptr(), self.stride, self.q.data_ptr(), self.o.data_ptr(),
+                          self.ws.data_ptr(), self.ws.numel(), 0, stream, timing)
+
+
+def solo_ms(call, stream, reps: int, kernel_only: bool) -> float:
+    ts = [Timing() for _ in range(reps + 1)]
+    torch.cuda.synchronize()
+    for t in ts:
+        call(stream, t.h)
+    torch.cuda.synchronize()
+    vals = [t.kernel_ms(0) if kernel_only else t.elapsed()[0] for t in ts[1:]]
+    for t in ts:
+        t.close()
+    return statistics.median(vals)
+
+
+def pair_slowdown(pre: PrefillCall, dec: DecodeCall, part: Partition, pre_ms: float, dec_ms: float) -> dict:
+    """Decode calls back to back on the decode CUs with prefill calls next to
+    them (decode enqueued first); the decode calls that ran entirely inside
+    the prefill window give the multiplexed latency."""
+    n_pre = min(256, max(1, math.ceil(3 * dec_ms / pre_ms)))
+    n_dec = math.ceil(n_pre * pre_ms / dec_ms) + 3
+    td = [Timing() for _ in range(n_dec)]
+    tp = [Timing() for _ in range(n_pre)]
+    torch.cuda.synchronize()
+    for t in td:
+        dec(part.decode_stream, t.h)
+    for t in tp:
+        pre(part.prefill_stream, t.h)
+    torch.cuda.synchronize()
+    ref = td[0].h
+    p0 = mw.mw_timing_offsets(tp[0].h, ref)[0]
+    p1 = mw.mw_timing_offsets(tp[-1].h, ref)[1]
+    inside = []
+    for t in td:
+        a, b = mw.mw_timing_offsets(t.h, ref)
+        if a >= p0 and b <= p1:
+            inside.append(t.elapsed()[0])
+    pre_mux = statistics.median(t.kernel_ms(0) for t in tp)
+    for t in td + tp:
+        t.close()
+    if not inside:
+        return {"decode_mux_ms": None, "slowdown": None, "prefill_mux_ms": pre_mux}
+    mux = statistics.median(inside)
+    return {"decode_mux_ms": mux, "slowdown": mux / dec_ms, "prefill_mux_ms": pre_mux,
+            "decode_calls_inside": len(inside)}
+
+
+def work_groups(sample, phase) -> int:
+    """Work-groups of the call (query blocks of 64 positions x kv heads for
+    prefill, chunks of 32 pages x kv heads for decode)."""
+    if phase == 0:
+        return (sample["n"] + 63) // 64 * HKV
+    return sum((L + 32 * PAGE - 1) // (32 * PAGE) for L in sample["lens"]) * HKV
+
+
+def fit_and_score(samples, train_filter, phase):
+    """Fits the library's predictor on the training samples; returns the
+    coefficients and the maximum relative deviation on training and held-out
+    samples per partition size."""
+    p = mw.mw_predictor_create()
+    out = {}
+    try:
+        for s in samples:
+            if not train_filter(s):
+                continue
+            if phase == 0:
+                mw.mw_predictor_add_prefill(p, s["cus"], [s["n"]], [s["r"]], s["ms"])
+            else:
+                mw.mw_predictor_add_decode(p, s["cus"], s["lens"], s["ms"])
+        mw.mw_predictor_fit(p)
+        for cus in sorted({s["cus"] for s in samples}):
+            th = mw.mw_predictor_coefficients(p, phase, cus)
+            dev = {"train": 0.0, "held_out": 0.0, "held_out_filling": 0.0}
+            for s in samples:
+                if s["cus"] != cus:
+                    continue
+                pred = (mw.mw_predictor_prefill_ms(p, cus, [s["n"]], [s["r"]]) if phase == 0
+                        else mw.mw_predictor_decode_ms(p, cus, s["lens"]))
+                s["pred_ms"] = pred
+                k = "train" if train_filter(s) else "held_out"
+                err = abs(pred - s["ms"]) / s["ms"]
+                dev[k] = max(dev[k], err)
+                # calls with at least one work-group per CU: the regime the
+                # linear-in-work models describe
+                s["fills_partition"] = work_groups(s, phase) >= cus
+                if k == "held_out" and s["fills_partition"]:
+                    dev["held_out_filling"] = max(dev["held_out_filling"], err)
+            out[cus] = {"theta": [float(x) for x in th], "max_dev": dev}
+    finally:
+        mw.mw_predictor_destroy(p)
+    return out
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--out", required=True)
+    ap.add_argument("--prefill-cus", default="64,128,192")
+    ap.add_argument("--reps", type=int, default=5)
+    ap.add_argument("--held-out", type=int, default=10, help="random held-out samples per partition and phase")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--quick", action="store_true", help="a small grid (functional check)")
+    args = ap.parse_args(argv)
+    torch.cuda.init()
+    grid_n = [1024, 4096, 16384]
+    grid_r = [0, 4096, 16384]
+    grid_bs = [8, 32, 128]
+    grid_L = [1024, 4096, 16384]
+    if args.quick:
+        grid_n, grid_r, grid_bs, grid_L = [128, 512, 1024], [0, 1024], [4, 16], [512, 2048]
+    rng = np.random.default_rng(args.seed)
+    pages = grid_bs[-1] * grid_L[-1] // PAGE + (grid_n[-1] + grid_r[-1]) // PAGE + 64
+    t_start = time.time()
+    pool = Pool(pages, args.seed)
+    log(f"[profiling] pool of {pages} pages ({2 * pages * HKV * PAGE * D * 2 / 1e9:.1f} GB)")
+    result = {"model": {"num_q_heads": HQ, "num_kv_heads": HKV, "head_dim": D, "page_size": PAGE},
+              "grid": {"prefill_new": grid_n, "prefill_reused": grid_r, "decode_batch": grid_bs,
+                       "decode_len": grid_L}, "prefill": [], "decode": [], "pairs": []}
+    try:
+        for pc in [int(x) for x in args.prefill_cus.split(",")]:
+            dc = 256 - pc
+            part = Partition(pc, dc)
+            try:
+                pre_pts = [(n, r, True) for n in grid_n for r in grid_r]
+                pre_pts += [(int(rng.integers(grid_n[0] // 2, grid_n[-1] + 1)),
+                             int(rng.integers(0, grid_r[-1] + 1)), False) for _ in range(args.held_out)]
+                pre_calls = {}
+                for n, r, grid in pre_pts:
+                    c = PrefillCall(pool, n, r)
+                    ms = solo_ms(c, part.prefill_stream, args.reps, kernel_only=True)
+                    result["prefill"].append({"cus": pc, "n": n, "r": r, "ms": ms, "grid": grid})
+                    if grid:
+                        pre_calls[(n, r)] = (c, ms)
+                dec_pts = [([L] * bs, True) for bs in grid_bs for L in grid_L]
+                for _ in range(args.held_out):
+                    bs = int(rng.integers(grid_bs[0] // 2, grid_bs[-1] * 3 // 4 + 1))  # fits the pool
+                    dec_pts.append((rng.integers(grid_L[0] // 2, grid_L[-1] + 1, bs).tolist(), False))
+                dec_calls = {}
+                for lens, grid in dec_pts:
+                    c = DecodeCall(pool, lens)
+                    ms = solo_ms(c, part.decode_stream, args.reps, kernel_only=False)
+                    result["decode"].append({"cus": dc, "lens": [int(x) for x in lens], "ms": ms, "grid": grid})
+                    if grid:
+                        dec_calls[(len(lens), lens[0])] = (c, ms)
+                log(f"[profiling] {pc}/{dc}: solo runs done ({time.time() - t_start:.0f}s)")
+                for (n, r), (pcall, pms) in pre_calls.items():
+                    for (bs, L), (dcall, dms) in dec_calls.items():
+                        res = pair_slowdown(pcall, dcall, part, pms, dms)
+                        res.update({"prefill_cus": pc, "prefill_new": n, "prefill_reused": r, "decode_batch": bs,
+                                    "decode_reused": bs * (L - 1), "prefill_solo_ms": pms, "decode_solo_ms": dms})
+                        result["pairs"].append(res)
+                log(f"[profiling] {pc}/{dc}: pairs done ({time.time() - t_start:.0f}s)")
+            finally:
+                part.close()
+    finally:
+        pool.close()
+    # solo-run predictor: fit on the grid, score on the held-out samples
+    result["predictor"] = {
+        "prefill": fit_and_score(result["prefill"], lambda s: s["grid"], 0),
+        "decode": fit_and_score(result["decode"], lambda s: s["grid"], 1)}
+    # contention guard from the pairs; worst-case estimate = prediction x guard
+    g = mw.mw_guard_create()
+    try:
+        for s in result["pairs"]:
+            if s["slowdown"] is not None:
+                mw.mw_guard_add(g, s["prefill_new"], s["prefill_reused"], s["decode_batch"], s["decode_reused"],
+                                s["prefill_cus"], s["slowdown"])
+        sl = [s["slowdown"] for s in result["pairs"] if s["slowdown"] is not None]
+        result["guard"] = {"pairs": len(result["pairs"]), "pairs_measured": len(sl),
+                           "max_slowdown": max(sl) if sl else None,
+                           "median_slowdown": statistics.median(sl) if sl else None}
+        per = {}
+        for s in result["pairs"]:
+            if s["slowdown"] is not None:
+                per.setdefault(s["prefill_cus"], []).append(s["slowdown"])
+        result["guard"]["max_by_prefill_cus"] = {str(k): max(v) for k, v in per.items()}
+    finally:
+        mw.mw_guard_destroy(g)
+    result["seconds"] = time.time() - t_start
+    with open(args.out, "w") as f:
+        json.dump(result, f, indent=1)
+    pr = result["predictor"]
+    log("[profiling] max relative deviation (held out): prefill " +
+        ", ".join(f"{c} CUs {100 * v['max_dev']['held_out']:.1f}%" for c, v in pr["prefill"].items()) +
+        "; decode " + ", ".join(f"{c} CUs {100 * v['max_dev']['held_out']:.1f}%" for c, v in pr["decode"].items()))
+    log(f"[profiling] guard: max slowdown {result['guard']['max_slowdown']}, {result['seconds']:.0f}s total")
+
+
+if __name__ == "__main__":
+    main()

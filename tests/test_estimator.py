@@ -1,0 +1,171 @@
+"""Contention-tolerant estimator (paper Sec. 3.3, 3.4): the oracle pinned to
+closed forms, then the library's host-side implementation against it."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import estimator as E
+from paper_2504_14489_amd import mw
+
+
+# ---------------------------------------------------------------- oracle pins
+def test_oracle_recovers_known_coefficients_exactly():
+    rng = np.random.default_rng(1)
+    th = np.array([3e-7, 1.5e-7, 2e-3, 0.05])
+    X, t = [], []
+    for _ in range(40):
+        bs = int(rng.integers(1, 4))
+        n = rng.integers(1, 8192, bs); r = rng.integers(0, 32768, bs)
+        X.append(E.prefill_features(n, r))
+        # Eq. (1) written out independently of prefill_features
+        t.append(th[0] * sum(int(a) ** 2 for a in n) + th[1] * sum(int(a) * int(b) for a, b in zip(n, r))
+                 + th[2] * int(n.sum()) + th[3])
+    np.testing.assert_allclose(E.fit_relative(np.array(X), np.array(t)), th, rtol=1e-9)
+    thd = np.array([2e-6, 4e-3, 0.03])
+    X, t = [], []
+    for _ in range(30):
+        L = rng.integers(1, 20000, int(rng.integers(1, 64)))
+        X.append(E.decode_features(L))
+        t.append(thd[0] * int((L - 1).sum()) + thd[1] * len(L) + thd[2])  # Eq. (2), r = L - 1
+    np.testing.assert_allclose(E.fit_relative(np.array(X), np.array(t)), thd, rtol=1e-9)
+
+
+def test_oracle_relative_weighting_closed_form():
+    # one constant term: argmin sum ((c - t)/t)^2 is sum(1/t) / sum(1/t^2), not mean(t)
+    t = np.array([1.0, 2.0, 4.0, 10.0])
+    c = E.fit_relative(np.ones((4, 1)), t)[0]
+    assert c == pytest.approx(np.sum(1 / t) / np.sum(1 / t ** 2), rel=1e-12)
+    assert abs(c - t.mean()) > 1.0
+
+
+def test_oracle_guard_cells_and_layers():
+    assert [E.cell(x, 4) for x in (0, 1, 2, 4, 5, 4096, 4097, 131072)] == [0, 0, 1, 1, 2, 6, 7, 9]
+    assert [E.cell(x, 2) for x in (1, 2, 3, 32, 33)] == [0, 1, 2, 5, 6]
+    cells = E.guard_build([((4096, 0, 32, 65536, 64), 1.10), ((3000, 0, 17, 50000, 64), 1.25),
+                           ((4096, 0, 32, 65536, 128), 1.05)])
+    assert E.guard_lookup(cells, (2049, 0, 20, 40000, 64)) == 1.25   # same cell: the maximum
+    assert E.guard_lookup(cells, (16, 16, 1, 1, 64)) == 1.25         # empty cell: partition max
+    assert E.guard_lookup(cells, (16, 16, 1, 1, 32)) == 1.25         # unknown partition: global max
+    assert E.guard_lookup({}, (1, 1, 1, 1, 64)) == 1.0
+    # Sec. 3.4: T_d = 30 ms next to a 1000 ms prefill of an 80-layer model -> 3 layers
+    assert E.prefill_layers(30.0, 1000.0, 80) == 3
+    assert E.prefill_layers(5000.0, 10.0, 32) == 32 and E.prefill_layers(1e-6, 10.0, 32) == 1
+
+
+# ---------------------------------------------------- library against oracle
+def _noisy_samples(rng, n_samples):
+    th = np.array([4e-7, 2e-7, 1e-3, 0.02])
+    out = []
+    for _ in range(n_samples):
+        bs = int(rng.integers(1, 4))
+        n = rng.integers(1, 4096, bs); r = rng.integers(0, 16384, bs)
+        t = float(E.prefill_features(n, r) @ th) * float(rng.uniform(0.9, 1.1))
+        out.append((n, r, t))
+    return out
+
+
+def test_predictor_fit_and_predictions_match_oracle():
+    rng = np.random.default_rng(7)
+    p = mw.mw_predictor_create()
+    try:
+        per_cus = {}
+        for cus in (64, 128):
+            smp = _noisy_samples(rng, 25)
+            per_cus[cus] = smp
+            for n, r, t in smp:
+                mw.mw_predictor_add_prefill(p, cus, n, r, t)
+        dsmp = []
+        for _ in range(20):
+            L = rng.integers(1, 9000, int(rng.integers(1, 48)))
+            t = (1e-5 * (L - 1).sum() + 2e-3 * len(L) + 0.01) * float(rng.uniform(0.92, 1.08))
+            dsmp.append((L, t))
+            mw.mw_predictor_add_decode(p, 192, L, t)
+        mw.mw_predictor_fit(p)
+        for cus, smp in per_cus.items():
+            X = np.array([E.prefill_features(n, r) for n, r, _ in smp]); t = np.array([s[2] for s in smp])
+            ref = E.fit_relative(X, t)
+            np.testing.assert_allclose(mw.mw_predictor_coefficients(p, 0, cus), ref, rtol=1e-8)
+            for n, r, _ in smp[:5]:
+                assert mw.mw_predictor_prefill_ms(p, cus, n, r) == pytest.approx(
+                    float(E.prefill_features(n, r) @ ref), rel=1e-9)
+        X = np.array([E.decode_features(L) for L, _ in dsmp]); t = np.array([s[1] for s in dsmp])
+        ref = E.fit_relative(X, t)
+        np.testing.assert_allclose(mw.mw_predictor_coefficients(p, 1, 192)[:3], ref, rtol=1e-8)
+        L = dsmp[0][0]
+        assert mw.mw_predictor_decode_ms(p, 192, L) == pytest.approx(float(E.decode_features(L) @ ref),
+                                                                      rel=1e-9)
+    finally:
+        mw.mw_predictor_destroy(p)
+
+
+def test_predictor_unexercised_term_and_errors():
+    p = mw.mw_predictor_create()
+    try:
+        with pytest.raises(mw.MWError) as ei:
+            mw.mw_predictor_fit(p)
+        assert ei.value.status == mw.MW_ERR_NOT_READY
+        rng = np.random.default_rng(3)
+        X, t = [], []
+        for _ in range(10):  # no reused tokens at all: the n*r term stays 0
+            n = rng.integers(1, 2048, 2)
+            tt = float(1e-6 * (n ** 2).sum() + 1e-3 * n.sum() + 0.05)
+            mw.mw_predictor_add_prefill(p, 32, n, [0, 0], tt)
+            X.append(E.prefill_features(n, [0, 0])); t.append(tt)
+        mw.mw_predictor_fit(p)
+        th = mw.mw_predictor_coefficients(p, 0, 32)
+        assert th[1] == 0.0
+        np.testing.assert_allclose(th, E.fit_relative(np.array(X), np.array(t)), rtol=1e-8, atol=1e-18)
+        with pytest.raises(mw.MWError) as ei:
+            mw.mw_predictor_prefill_ms(p, 64, [10], [0])   # no model for 64 CUs
+        assert ei.value.status == mw.MW_ERR_NOT_READY
+        for bad in (lambda: mw.mw_predictor_add_prefill(p, 32, [0], [0], 1.0),
+                    lambda: mw.mw_predictor_add_prefill(p, 32, [5], [-1], 1.0),
+                    lambda: mw.mw_predictor_add_prefill(p, 32, [5], [0], -1.0),
+                    lambda: mw.mw_predictor_add_prefill(p, 32, [5], [0], float("nan")),
+                    lambda: mw.mw_predictor_add_decode(p, 0, [5], 1.0),
+                    lambda: mw.mw_predictor_add_decode(p, 32, [0], 1.0)):
+            with pytest.raises(mw.MWError) as ei:
+                bad()
+            assert ei.value.status == mw.MW_ERR_INVALID_ARG
+    finally:
+        mw.mw_predictor_destroy(p)
+
+
+def test_guard_matches_oracle():
+    rng = np.random.default_rng(11)
+    g = mw.mw_guard_create()
+    try:
+        samples = []
+        for _ in range(300):
+            key = (int(rng.choice([512, 2048, 8192, 30000])), int(rng.choice([0, 1024, 16384])),
+                   int(rng.integers(1, 200)), int(rng.integers(0, 2_000_000)), int(rng.choice([64, 128, 192])))
+            s = float(rng.uniform(0.98, 1.3))
+            samples.append((key, s))
+            mw.mw_guard_add(g, *key, s)
+        cells = E.guard_build(samples)
+        for _ in range(500):
+            key = (int(rng.integers(0, 40000)), int(rng.integers(0, 40000)), int(rng.integers(1, 300)),
+                   int(rng.integers(0, 3_000_000)), int(rng.choice([32, 64, 128, 192])))
+            assert mw.mw_guard_lookup(g, *key) == E.guard_lookup(cells, key)
+        with pytest.raises(mw.MWError):
+            mw.mw_guard_add(g, 1, 1, 0, 1, 64, 1.1)
+        with pytest.raises(mw.MWError):
+            mw.mw_guard_add(g, 1, 1, 1, 1, 64, 0.0)
+    finally:
+        mw.mw_guard_destroy(g)
+    g = mw.mw_guard_create()
+    try:
+        assert mw.mw_guard_lookup(g, 1, 1, 1, 1, 64) == 1.0
+    finally:
+        mw.mw_guard_destroy(g)
+
+
+def test_prefill_layers_matches_oracle():
+    rng = np.random.default_rng(5)
+    for _ in range(200):
+        td, tp, nl = float(rng.uniform(0.01, 50)), float(rng.uniform(0.05, 5000)), int(rng.integers(1, 128))
+        assert mw.mw_prefill_layers(td, tp, nl) == E.prefill_layers(td, tp, nl)
+    for bad in ((0.0, 1.0, 32), (1.0, 0.0, 32), (1.0, 1.0, 0), (math.inf, 1.0, 32)):
+        with pytest.raises(mw.MWError):
+            mw.mw_prefill_layers(*bad)
