@@ -81,12 +81,21 @@ __device__ inline float dot2_ones(uint32_t p, float acc) {
     return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p), one, acc, false);
 }
 
-// max(x, x of lane l ^ 32): the swap hands lanes 0..31 the upper half and
-// lanes 32..63 the lower half, so the two results hold both values everywhere.
+// NaN-propagating maximum: a single v_maximum3_f32 on gfx950, with no
+// canonicalisation of the MFMA results it reads.
+__device__ inline float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
+// max(x, x of lane l ^ 32).  v_permlane32_swap exchanges lanes 32..63 of its
+// first operand with lanes 0..31 of its second, so with x in both operands
+// one result holds the lower half's values in every lane and the other the
+// upper half's.  Inline assembly because this compiler takes the builtin's
+// second result to be its first (the maximum would then cover only half the
+// keys); the s_nop covers the two wait states the swap needs after a vector
+// instruction writes its operands.
 __device__ inline float max_xor32(float x) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, x),
-                                                    __builtin_bit_cast(uint32_t, x), false, false);
-    return fmaxf(__builtin_bit_cast(float, r[0]), __builtin_bit_cast(float, r[1]));
+    float a = x, b = x;
+    asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+    return vmax(a, b);
 }
 
 // Transposing LDS read: within each 16-lane group, lane s points at 4
@@ -295,14 +304,13 @@ k_prefill_attn(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ 
         float m8[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j)
-            m8[j] = fmaxf(fmaxf(sacc[j >> 2][4 * (j & 3)], sacc[j >> 2][4 * (j & 3) + 1]),
-                          fmaxf(sacc[j >> 2][4 * (j & 3) + 2], sacc[j >> 2][4 * (j & 3) + 3]));
-        float mx = fmaxf(fmaxf(fmaxf(m8[0], m8[1]), fmaxf(m8[2], m8[3])),
-                         fmaxf(fmaxf(m8[4], m8[5]), fmaxf(m8[6], m8[7])));
+            m8[j] = vmax(vmax(sacc[j >> 2][4 * (j & 3)], sacc[j >> 2][4 * (j & 3) + 1]),
+                         vmax(sacc[j >> 2][4 * (j & 3) + 2], sacc[j >> 2][4 * (j & 3) + 3]));
+        float mx = vmax(vmax(vmax(m8[0], m8[1]), vmax(m8[2], m8[3])), vmax(vmax(m8[4], m8[5]), vmax(m8[6], m8[7])));
         mx = max_xor32(mx);  // lanes l and l^32 hold the same query
         const float m_tile = mx * scale_log2;
         if (__builtin_amdgcn_ballot_w64(m_tile > m_run + kRescaleLog2) != 0) {
-            const float m_new = fmaxf(m_run, m_tile);
+            const float m_new = vmax(m_run, m_tile);
             const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
             m_run = m_new;
             l_run *= alpha;

@@ -101,3 +101,25 @@ def test_decode_equals_last_prefill_row():
     assert_close(dec[None], ref[None], "decode")
     diff = np.abs(W.bf16_bits_to_f32(pre) - W.bf16_bits_to_f32(dec))
     assert diff.max() <= 2e-2
+
+
+def test_decode_wide_score_range():
+    """Keys scaled by 32 against Q scaled by 8, placed in different chunks and
+    in both halves of an 8-key group: the split maxima and the combine must
+    keep every 2^(s - m) finite."""
+    say("decode wide score range")
+    from paper_2504_14489_amd.device import bits_to_f32
+    cfg = W.custom_config(hq=8, hkv=2, pre_chunks=((0, 1),), dec_batch=3, seed=78)
+    wl = W.make_workload(cfg, q_scale=8.0, dec_lens=[700, 1500, 33])
+    k = wl.k_pool.copy()
+    for b, positions in enumerate([[5, 500, 699], [6, 600, 1200, 1499], [1, 32]]):
+        for t in positions:
+            page, slot = wl.dec_bt[b, t // 16], t % 16
+            row = bits_to_f32(k[page, :, slot, :]) * 32.0
+            k[page, :, slot, :] = (row.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    wl = W.Workload(cfg=wl.cfg, k_pool=k, v_pool=wl.v_pool, nan_page=wl.nan_page, pre_len=wl.pre_len,
+                    pre_bt=wl.pre_bt, q_pre=wl.q_pre, dec_lens=wl.dec_lens, dec_bt=wl.dec_bt,
+                    q_dec=wl.q_dec, perm=wl.perm)
+    got = run_decode(wl)
+    ref = oracle.decode(wl.q_dec, wl.k_pool, wl.v_pool, wl.dec_bt, wl.dec_lens)
+    assert_close(got, ref, "decode wide score range")

@@ -147,3 +147,33 @@ def test_prefill_same_result_on_any_cu_count():
     rows = [0, 63, 64, 255, 511]
     ref = oracle.prefill(wl.q_pre[:512], wl.k_pool, wl.v_pool, wl.pre_bt, 0)
     assert_close(outs[0][rows], ref[rows], "split independence rows")
+
+
+def _scale_keys(wl, bt, positions, factor):
+    """Multiplies the K rows of the given logical positions (all kv heads) by a
+    power of two, exactly in bf16."""
+    from paper_2504_14489_amd.device import bits_to_f32
+    k = wl.k_pool.copy()
+    for t in positions:
+        page, slot = bt[t // 16], t % 16
+        row = bits_to_f32(k[page, :, slot, :]) * factor
+        k[page, :, slot, :] = (row.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    return W.Workload(cfg=wl.cfg, k_pool=k, v_pool=wl.v_pool, nan_page=wl.nan_page, pre_len=wl.pre_len,
+                      pre_bt=wl.pre_bt, q_pre=wl.q_pre, dec_lens=wl.dec_lens, dec_bt=wl.dec_bt,
+                      q_dec=wl.q_dec, perm=wl.perm)
+
+
+def test_prefill_wide_score_range():
+    """A few keys scaled by 32 against Q scaled by 8 spread the scaled scores
+    over hundreds of log2 units, with the largest in either half of a
+    score accumulator's lanes: the running maximum must cover both halves (a
+    reference taken from half the keys overflows 2^(s - m)), and the late large
+    keys force the lazy rescale."""
+    say("prefill wide score range")
+    cfg = W.custom_config(hq=8, hkv=2, pre_chunks=((0, 200),), dec_batch=1, dec_len_lo=1,
+                          dec_len_hi=2, seed=77)
+    wl = _scale_keys(W.make_workload(cfg, q_scale=8.0), W.make_workload(cfg).pre_bt,
+                     [4, 5, 70, 131, 150, 199], 32.0)
+    got = run_prefill(wl, 0, 200)
+    ref = oracle.prefill(wl.q_pre[:200], wl.k_pool, wl.v_pool, wl.pre_bt, 0)
+    assert_close(got, ref, "prefill wide score range")
