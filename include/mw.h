@@ -231,9 +231,11 @@ mw_status mw_prefill_attn(const mw_kv_pool *pool, const mw_attn_shape *shape, in
                           void *d_out, mw_stream stream, mw_timing *timing);
 
 /* Decode is split over chunks of `chunk_pages` pages of each sequence (a
- * multiple of 8 in [8, 256]; 0 = default 32) and merged by a second kernel
- * (log-sum-exp combine).  The
- * split depends only on the lengths, never on page ids.
+ * multiple of 8 in [8, 256]; 0 = chosen from the lengths: the largest of 128,
+ * 64 and 32 that still gives at least 1024 (chunk, kv head) work units) and
+ * merged by a second kernel (log-sum-exp combine).  The split depends only on
+ * the lengths, never on page ids; pass the same chunk_pages (and lengths) to
+ * both calls.
  * Workspace bytes for a call with these lengths: */
 mw_status mw_decode_workspace_size(const mw_attn_shape *shape, int32_t batch,
                                    const int32_t *h_seq_lens, int32_t chunk_pages,

@@ -44,7 +44,11 @@ constexpr int VSTR = 144;                     // LDS V row stride (bf16): confli
 constexpr int kVBufElems = 16 * kPair * VSTR; // one wave's V buffer
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kRescaleLog2 = 8.f;
-constexpr int kDefaultChunkPages = 32;
+// chunk_pages = 0: the largest of 128, 64, 32 pages that still gives at least
+// kAutoMinUnits work-groups (longer chunks amortise each work-group's set-up
+// and merge; enough work-groups keep every CU of a partition streaming)
+constexpr int kAutoChunks[3] = {128, 64, 32};
+constexpr int64_t kAutoMinUnits = 1024;
 
 __device__ inline uint16_t to_bf16(float f) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f)); }
 __device__ inline uint32_t cvt2(float a, float b) {
@@ -333,6 +337,7 @@ k_decode_combine(uint16_t *__restrict__ out, const int32_t *__restrict__ seq_len
 
 struct Plan {
     int64_t units;
+    int chunk_pages;
     size_t off_ml, off_cbase, bytes;
 };
 
@@ -347,16 +352,29 @@ mw_status plan_decode(const mw_attn_shape *shape, int32_t batch, const int32_t *
         return fail(MW_ERR_INVALID_ARG, "%s: num_q_heads must be a positive multiple of num_kv_heads", who);
     if (shape->num_q_heads / shape->num_kv_heads > 16)
         return fail(MW_ERR_UNSUPPORTED, "%s: at most 16 query heads per kv head", who);
-    if (chunk_pages < 8 || chunk_pages > 256 || chunk_pages % 8)
+    if (chunk_pages != 0 && (chunk_pages < 8 || chunk_pages > 256 || chunk_pages % 8))
         return fail(MW_ERR_UNSUPPORTED, "%s: chunk_pages must be a multiple of 8 in [8, 256] (or 0)", who);
-    int64_t chunks = 0;
     for (int32_t b = 0; b < batch; ++b) {
         const int32_t L = h_seq_lens[b];
         if (L < 1 || (bt_stride > 0 && static_cast<int64_t>(L) > static_cast<int64_t>(bt_stride) * kPageSize))
             return fail(MW_ERR_INVALID_ARG, "%s: sequence %d has length %d (table holds %d pages)", who, b,
                         L, bt_stride);
-        chunks += ((L + kPageSize - 1) / kPageSize + chunk_pages - 1) / chunk_pages;
     }
+    auto count = [&](int ch) {
+        int64_t n = 0;
+        for (int32_t b = 0; b < batch; ++b) n += ((h_seq_lens[b] + kPageSize - 1) / kPageSize + ch - 1) / ch;
+        return n;
+    };
+    if (chunk_pages == 0) {
+        chunk_pages = kAutoChunks[2];
+        for (int ch : kAutoChunks)
+            if (count(ch) * shape->num_kv_heads >= kAutoMinUnits) {
+                chunk_pages = ch;
+                break;
+            }
+    }
+    plan->chunk_pages = chunk_pages;
+    const int64_t chunks = count(chunk_pages);
     const int group = shape->num_q_heads / shape->num_kv_heads;
     plan->units = chunks * shape->num_kv_heads;
     const size_t o_bytes = align256(static_cast<size_t>(plan->units) * group * kHeadDim * 4);
@@ -385,8 +403,7 @@ mw_status mw_decode_workspace_size(const mw_attn_shape *shape, int32_t batch, co
                                    int32_t chunk_pages, size_t *bytes) {
     if (!bytes) return fail(MW_ERR_INVALID_ARG, "mw_decode_workspace_size: bytes is NULL");
     Plan pl;
-    mw_status st = plan_decode(shape, batch, h_seq_lens, chunk_pages ? chunk_pages : kDefaultChunkPages, 0, &pl,
-                               "mw_decode_workspace_size");
+    mw_status st = plan_decode(shape, batch, h_seq_lens, chunk_pages, 0, &pl, "mw_decode_workspace_size");
     if (st != MW_OK) return st;
     *bytes = pl.bytes;
     return MW_OK;
@@ -398,10 +415,10 @@ mw_status mw_decode_attn(const mw_kv_pool *pool, const mw_attn_shape *shape, int
                          size_t workspace_bytes, int32_t chunk_pages, mw_stream stream, mw_timing *timing) {
     const char *who = "mw_decode_attn";
     if (!pool || bt_stride < 1) return fail(MW_ERR_INVALID_ARG, "%s: bad pool or bt_stride", who);
-    if (chunk_pages == 0) chunk_pages = kDefaultChunkPages;
     Plan pl;
     mw_status st = plan_decode(shape, batch, h_seq_lens, chunk_pages, bt_stride, &pl, who);
     if (st != MW_OK) return st;
+    chunk_pages = pl.chunk_pages;
     if (!(shape->scale > 0.f) || !(shape->scale < INFINITY))
         return fail(MW_ERR_INVALID_ARG, "%s: scale must be positive and finite", who);
     if (shape->num_kv_heads != pool->desc.num_kv_heads)
