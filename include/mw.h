@@ -319,6 +319,114 @@ mw_status mw_guard_lookup(const mw_guard *g, const mw_guard_key *key, double *sl
  * the result is clamped to [1, N_T].  Times > 0 and finite, n_layers >= 1. */
 mw_status mw_prefill_layers(double t_decode_ms, double t_prefill_ms, int32_t n_layers, int32_t *n_pl);
 
+/* ------------------------------------------------------------------------ *
+ * Bubble-less multiplex engine (paper Sec. 3.2, "Bubble-less Multiplex
+ * Engine"): a group of CU partitions created once, and a host loop that
+ * feeds decode iterations and prefill layers to their streams.
+ *
+ * The paper's engine splits prefill into layers, launches N_PL layers at a
+ * time next to each decode iteration, polls events instead of blocking
+ * ("query-based synchronization") and moves the remaining prefill layers to
+ * a new partition when decode ends.  Here a decode iteration is
+ * `decode_layers` decode attention calls and the prefill job is
+ * `prefill_layers` prefill attention calls (one per transformer layer, made
+ * with the same arguments each time: the attention hot path of the layers,
+ * not the rest of the model).
+ *
+ * mw_engine_create: one partition per entry of prefill_cus[0..n) (prefill on
+ *     that many CUs, decode on the device's other CUs; multiples of 8), plus
+ *     a stream on the whole device; 1 <= n <= 16.  The device memory the
+ *     group takes (free memory before minus after) and the creation time are
+ *     reported by mw_engine_memory.
+ * mw_engine_streams: the prefill and decode streams of partition `config`
+ *     (config = -1: the whole-device stream in both).
+ * mw_engine_run: one multiplexed run on partition plan->config; blocks until
+ *     every call it launched has completed, then fills `stats`.  Device
+ *     buffers are the caller's, as for mw_decode_attn / mw_prefill_attn;
+ *     lengths arrays are host copies read at launch time.
+ *   policy MW_ENGINE_BLOCKING: launch decode iteration 0, then the whole
+ *     prefill job, and wait (blocking) for each decode iteration before
+ *     launching the next; the prefill keeps its partition to the end.
+ *   policy MW_ENGINE_POLLED: launch decode iteration 0 and N_PL =
+ *     plan->layers_per_launch prefill layers; then poll: a finished decode
+ *     iteration is followed at once by the next, and prefill layers are
+ *     topped up N_PL at a time whenever fewer than N_PL are queued; with
+ *     plan->switch_on_decode_end the layers launched after the last decode
+ *     iteration ends go to the whole-device stream (ordered after the
+ *     earlier layers by a cross-stream event wait).
+ * Stats (device times from HIP events around every call, in ms from the
+ * first launch): each stream's busy time (sum of its calls) and bubble ratio
+ * (1 - busy / its first-start-to-last-end window), their mean, the longest
+ * gap between consecutive decode iterations, the prefill job's end, and at a
+ * partition switch the gap on the prefill timeline and the host time of the
+ * switch itself (the cross-stream wait and the change of stream, not the
+ * launches that follow).  Each event pair adds a marker packet per call, so
+ * the bubbles include that marker time (a few microseconds per call).
+ * Errors: MW_ERR_INVALID_ARG for a NULL pointer, a config outside [0, n), a
+ * count below 1 or an unknown policy (nothing launched); the argument
+ * checks of mw_decode_attn / mw_prefill_attn on the first launch; MW_ERR_HIP
+ * for a HIP failure, returned after every launched call has completed.  The
+ * engine owns its streams and events only; one run at a time per engine. */
+typedef struct mw_engine mw_engine;
+enum { MW_ENGINE_BLOCKING = 0, MW_ENGINE_POLLED = 1 };
+typedef struct {
+    const mw_kv_pool *pool;
+    mw_attn_shape shape;
+    int32_t batch;
+    const int32_t *h_seq_lens, *d_seq_lens, *d_block_table;
+    int32_t bt_stride;
+    const void *d_q;
+    void *d_out, *d_workspace;
+    size_t workspace_bytes;
+    int32_t chunk_pages;
+} mw_decode_args;
+typedef struct {
+    const mw_kv_pool *pool;
+    mw_attn_shape shape;
+    int32_t batch;
+    const int32_t *h_new_lens, *h_prefix_lens, *d_qo_indptr, *d_prefix_lens, *d_block_table;
+    int32_t bt_stride;
+    const void *d_q;
+    void *d_out;
+} mw_prefill_args;
+typedef struct {
+    int32_t config;             /* partition index, 0 <= config < n */
+    int32_t decode_iters;       /* >= 1 */
+    int32_t decode_layers;      /* decode calls per iteration, >= 1 */
+    int32_t prefill_layers;     /* prefill calls of the job, >= 1 */
+    int32_t layers_per_launch;  /* N_PL, >= 1 (polled policy) */
+    int32_t policy;             /* MW_ENGINE_BLOCKING or MW_ENGINE_POLLED */
+    int32_t switch_on_decode_end;
+} mw_engine_plan;
+typedef struct {
+    double wall_ms;                       /* first launch to last completion */
+    double decode_busy_ms, prefill_busy_ms;
+    double decode_bubble, prefill_bubble, bubble_ratio;
+    double decode_gap_ms_max;             /* longest idle gap between decode iterations */
+    double decode_iter_ms_mean;           /* decode iteration, first call start to last call end */
+    double prefill_end_ms;                /* completion of the last prefill layer */
+    double switch_gap_ms;                 /* prefill timeline gap at the switch; -1 if none */
+    double switch_host_us;                /* host time of the switch; -1 if none */
+    double host_launch_ms;                /* host time spent launching */
+    int32_t prefill_batches;              /* launch decisions that launched prefill layers */
+    int32_t switched_layers;              /* prefill layers run on the whole device */
+} mw_engine_stats;
+mw_status mw_engine_create(int32_t device, const int32_t *prefill_cus, int32_t n, mw_engine **out);
+mw_status mw_engine_destroy(mw_engine *eng);
+mw_status mw_engine_streams(const mw_engine *eng, int32_t config, mw_stream *prefill, mw_stream *decode);
+mw_status mw_engine_memory(const mw_engine *eng, int64_t *device_bytes, double *create_ms);
+mw_status mw_engine_run(mw_engine *eng, const mw_decode_args *dec, const mw_prefill_args *pre,
+                        const mw_engine_plan *plan, mw_engine_stats *stats);
+
+/* Per-call timeline of the last mw_engine_run on `eng`: phase 0 = decode
+ * calls, 1 = prefill calls, in launch order.  Writes min(n_calls, capacity)
+ * rows of three doubles (start ms, end ms, 1 if the call ran on the whole
+ * device after a switch, else 0), times relative to the run's reference
+ * event, to the host array `out`; *n_calls receives the number of calls.
+ * capacity 0 only queries the count. */
+mw_status mw_engine_timeline(const mw_engine *eng, int32_t phase, double *out, int32_t capacity,
+                             int32_t *n_calls);
+
 #ifdef __cplusplus
 }
 #endif

@@ -124,6 +124,36 @@ class DeviceWorkload:
                             timing)
 
 
+    # ------------------------------------------------------------ engine --
+    def engine_args(self, chunk_pages: int = 0):
+        """(decode, prefill) argument dicts for :func:`mw.mw_engine_run`: one
+        decode call over every sequence, and one prefill call whose batch holds
+        every prefill chunk (chunk j attends to its prefix and causally to
+        itself, so the batch equals running the chunks in order)."""
+        c = self.cfg
+        chunks = list(c.pre_chunks)
+        for (r0, n0), (r1, _) in zip(chunks, chunks[1:]):
+            if r1 != r0 + n0:
+                raise ValueError("prefill chunks must be contiguous")
+        if "engine" not in self._pre_args:
+            indptr = np.concatenate([[0], np.cumsum([n for _, n in chunks])])
+            bt = np.repeat(self.wl.pre_bt[None, :], len(chunks), axis=0)
+            self._pre_args["engine"] = (_dev32(indptr, self.device), _dev32([r for r, _ in chunks], self.device),
+                                        _dev32(bt, self.device))
+        indptr, pref, bt = self._pre_args["engine"]
+        r0 = chunks[0][0]
+        ws = self.workspace(chunk_pages)
+        shape = dict(hq=self.hq, hkv=self.hkv, head_dim=self.d, scale=self.scale)
+        dec = dict(pool=self.pool, seq_lens=self.dec_lens, d_seq_lens=self.d_dec_lens.data_ptr(),
+                   d_block_table=self.dec_bt.data_ptr(), bt_stride=self.dec_bt.shape[1],
+                   d_q=self.q_dec.data_ptr(), d_out=self.o_dec.data_ptr(), d_workspace=ws.data_ptr(),
+                   workspace_bytes=ws.numel(), chunk_pages=chunk_pages, **shape)
+        pre = dict(pool=self.pool, new_lens=[n for _, n in chunks], prefix_lens=[r for r, _ in chunks],
+                   d_qo_indptr=indptr.data_ptr(), d_prefix_lens=pref.data_ptr(), d_block_table=bt.data_ptr(),
+                   bt_stride=bt.shape[1], d_q=self.q_pre[r0].data_ptr(), d_out=self.o_pre[r0].data_ptr(), **shape)
+        return dec, pre
+
+
 class Timing:
     """Owns an mw_timing handle."""
 

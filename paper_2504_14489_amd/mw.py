@@ -53,6 +53,43 @@ class _AttnShape(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("scale", ctypes.c_float)]
 
 
+class _DecodeArgs(ctypes.Structure):
+    _fields_ = [("pool", ctypes.c_void_p), ("shape", _AttnShape), ("batch", ctypes.c_int32),
+                ("h_seq_lens", ctypes.c_void_p), ("d_seq_lens", ctypes.c_void_p),
+                ("d_block_table", ctypes.c_void_p), ("bt_stride", ctypes.c_int32),
+                ("d_q", ctypes.c_void_p), ("d_out", ctypes.c_void_p), ("d_workspace", ctypes.c_void_p),
+                ("workspace_bytes", ctypes.c_size_t), ("chunk_pages", ctypes.c_int32)]
+
+
+class _PrefillArgs(ctypes.Structure):
+    _fields_ = [("pool", ctypes.c_void_p), ("shape", _AttnShape), ("batch", ctypes.c_int32),
+                ("h_new_lens", ctypes.c_void_p), ("h_prefix_lens", ctypes.c_void_p),
+                ("d_qo_indptr", ctypes.c_void_p), ("d_prefix_lens", ctypes.c_void_p),
+                ("d_block_table", ctypes.c_void_p), ("bt_stride", ctypes.c_int32),
+                ("d_q", ctypes.c_void_p), ("d_out", ctypes.c_void_p)]
+
+
+class EnginePlan(ctypes.Structure):
+    """mw_engine_plan (policy: MW_ENGINE_BLOCKING or MW_ENGINE_POLLED)."""
+    _fields_ = [("config", ctypes.c_int32), ("decode_iters", ctypes.c_int32),
+                ("decode_layers", ctypes.c_int32), ("prefill_layers", ctypes.c_int32),
+                ("layers_per_launch", ctypes.c_int32), ("policy", ctypes.c_int32),
+                ("switch_on_decode_end", ctypes.c_int32)]
+
+
+class EngineStats(ctypes.Structure):
+    _fields_ = [(f, ctypes.c_double) for f in (
+        "wall_ms", "decode_busy_ms", "prefill_busy_ms", "decode_bubble", "prefill_bubble", "bubble_ratio",
+        "decode_gap_ms_max", "decode_iter_ms_mean", "prefill_end_ms", "switch_gap_ms", "switch_host_us",
+        "host_launch_ms")] + [("prefill_batches", ctypes.c_int32), ("switched_layers", ctypes.c_int32)]
+
+    def as_dict(self) -> dict:
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
+MW_ENGINE_BLOCKING = 0
+MW_ENGINE_POLLED = 1
+
 _lib = None
 _P = ctypes.c_void_p
 _I = ctypes.c_int32
@@ -106,6 +143,13 @@ _SIGNATURES = {
     "mw_guard_add": ([_P, ctypes.POINTER(GuardKey), ctypes.c_double], _I),
     "mw_guard_lookup": ([_P, ctypes.POINTER(GuardKey), _PD], _I),
     "mw_prefill_layers": ([ctypes.c_double, ctypes.c_double, _I, _PI], _I),
+    "mw_engine_create": ([_I, _PI, _I, ctypes.POINTER(_P)], _I),
+    "mw_engine_destroy": ([_P], _I),
+    "mw_engine_streams": ([_P, _I, ctypes.POINTER(_P), ctypes.POINTER(_P)], _I),
+    "mw_engine_memory": ([_P, ctypes.POINTER(ctypes.c_int64), _PD], _I),
+    "mw_engine_run": ([_P, ctypes.POINTER(_DecodeArgs), ctypes.POINTER(_PrefillArgs),
+                       ctypes.POINTER(EnginePlan), ctypes.POINTER(EngineStats)], _I),
+    "mw_engine_timeline": ([_P, _I, _PD, _I, _PI], _I),
 }
 
 EXPORTED = tuple(_SIGNATURES)
@@ -408,3 +452,57 @@ def mw_prefill_layers(t_decode_ms: float, t_prefill_ms: float, n_layers: int) ->
     out = ctypes.c_int32()
     _check(load().mw_prefill_layers(t_decode_ms, t_prefill_ms, n_layers, ctypes.byref(out)))
     return out.value
+
+
+# ---- multiplex engine
+
+def mw_engine_create(device: int, prefill_cus) -> ctypes.c_void_p:
+    pc = _i32(prefill_cus)
+    out = _P()
+    _check(load().mw_engine_create(device, _pi(pc), len(pc), ctypes.byref(out)))
+    return out
+
+
+def mw_engine_destroy(eng):
+    _check(load().mw_engine_destroy(eng))
+
+
+def mw_engine_streams(eng, config: int) -> Tuple[int, int]:
+    p, d = _P(), _P()
+    _check(load().mw_engine_streams(eng, config, ctypes.byref(p), ctypes.byref(d)))
+    return p.value or 0, d.value or 0
+
+
+def mw_engine_memory(eng) -> Tuple[int, float]:
+    b, ms = ctypes.c_int64(), ctypes.c_double()
+    _check(load().mw_engine_memory(eng, ctypes.byref(b), ctypes.byref(ms)))
+    return b.value, ms.value
+
+
+def mw_engine_run(eng, dec: dict, pre: dict, plan: EnginePlan) -> dict:
+    """dec: pool, hq, hkv, head_dim, scale, seq_lens (host), d_seq_lens, d_block_table,
+    bt_stride, d_q, d_out, d_workspace, workspace_bytes, chunk_pages;
+    pre: pool, hq, hkv, head_dim, scale, new_lens, prefix_lens (host), d_qo_indptr,
+    d_prefix_lens, d_block_table, bt_stride, d_q, d_out.  Returns the stats as a dict."""
+    sl = _i32(dec["seq_lens"])
+    nl, pl = _i32(pre["new_lens"]), _i32(pre["prefix_lens"])
+    da = _DecodeArgs(_h(dec["pool"]), _shape(dec["hq"], dec["hkv"], dec["head_dim"], dec["scale"]), len(sl),
+                     sl.ctypes.data, _h(dec["d_seq_lens"]), _h(dec["d_block_table"]), dec["bt_stride"],
+                     _h(dec["d_q"]), _h(dec["d_out"]), _h(dec["d_workspace"]), dec["workspace_bytes"],
+                     dec.get("chunk_pages", 0))
+    pa = _PrefillArgs(_h(pre["pool"]), _shape(pre["hq"], pre["hkv"], pre["head_dim"], pre["scale"]), len(nl),
+                      nl.ctypes.data, pl.ctypes.data, _h(pre["d_qo_indptr"]), _h(pre["d_prefix_lens"]),
+                      _h(pre["d_block_table"]), pre["bt_stride"], _h(pre["d_q"]), _h(pre["d_out"]))
+    st = EngineStats()
+    _check(load().mw_engine_run(eng, ctypes.byref(da), ctypes.byref(pa), ctypes.byref(plan), ctypes.byref(st)))
+    return st.as_dict()
+
+
+def mw_engine_timeline(eng, phase: int) -> np.ndarray:
+    """[n_calls][3] float64: start ms, end ms, on-whole-device flag."""
+    n = ctypes.c_int32()
+    _check(load().mw_engine_timeline(eng, phase, None, 0, ctypes.byref(n)))
+    out = np.zeros((n.value, 3), dtype=np.float64)
+    if n.value:
+        _check(load().mw_engine_timeline(eng, phase, out.ctypes.data_as(_PD), n.value, ctypes.byref(n)))
+    return out

@@ -155,3 +155,52 @@ def test_timing_not_ready(lib):
         assert mw.mw_timing_kernels(t) == 0
     finally:
         mw.mw_timing_destroy(t)
+
+
+def test_engine_validation_without_a_device(lib):
+    with pytest.raises(mw.MWError) as e:
+        mw.mw_engine_create(0, [], )
+    assert e.value.status == mw.MW_ERR_INVALID_ARG
+    with pytest.raises(mw.MWError) as e:
+        mw.mw_engine_create(0, [64] * 17)
+    assert e.value.status == mw.MW_ERR_INVALID_ARG
+    with pytest.raises(mw.MWError) as e:
+        mw.mw_engine_streams(None, 0)
+    assert e.value.status == mw.MW_ERR_INVALID_ARG
+    with pytest.raises(mw.MWError) as e:
+        mw.mw_engine_memory(None)
+    assert e.value.status == mw.MW_ERR_INVALID_ARG
+    mw.mw_engine_destroy(None)
+    plan = mw.EnginePlan(0, 1, 1, 1, 1, mw.MW_ENGINE_POLLED, 1)
+    dec = dict(pool=None, hq=8, hkv=2, head_dim=128, scale=0.1, seq_lens=[5], d_seq_lens=0, d_block_table=0,
+               bt_stride=1, d_q=0, d_out=0, d_workspace=0, workspace_bytes=0)
+    pre = dict(pool=None, hq=8, hkv=2, head_dim=128, scale=0.1, new_lens=[5], prefix_lens=[0], d_qo_indptr=0,
+               d_prefix_lens=0, d_block_table=0, bt_stride=1, d_q=0, d_out=0)
+    with pytest.raises(mw.MWError) as e:
+        mw.mw_engine_run(None, dec, pre, plan)
+    assert e.value.status == mw.MW_ERR_INVALID_ARG
+
+
+def test_engine_structs_match_the_header(tmp_path):
+    """ctypes layouts of the engine's argument, plan and stats structs agree
+    with what a C compiler makes of the header."""
+    import subprocess
+    structs = {"mw_decode_args": mw._DecodeArgs, "mw_prefill_args": mw._PrefillArgs,
+               "mw_engine_plan": mw.EnginePlan, "mw_engine_stats": mw.EngineStats}
+    lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "mw.h"', "int main(void) {"]
+    for cname, cls in structs.items():
+        lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')
+        for f, _ in cls._fields_:
+            lines.append(f'printf("{cname} {f} %zu\\n", offsetof({cname}, {f}));')
+    lines.append("return 0; }")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    inc = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+    subprocess.run(["gcc", "-std=c11", "-I", inc, str(src), "-o", str(exe)], check=True)
+    got = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    for line in filter(None, got):
+        cname, field, val = line.split()
+        cls = structs[cname]
+        want = ctypes.sizeof(cls) if field == "size" else getattr(cls, field).offset
+        assert int(val) == want, (cname, field, val, want)

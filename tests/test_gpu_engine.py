@@ -1,0 +1,131 @@
+"""The multiplex engine's host loop (paper Sec. 3.2): blocking and polled
+coordination, layer-wise prefill launches and the switch to the whole device
+must leave every output identical to one plain call, and its timeline
+statistics must describe what ran."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2504_14489_amd import mw, workloads as W
+from paper_2504_14489_amd.device import DeviceWorkload, to_bits
+from paper_2504_14489_amd.engine import Engine
+import oracle
+from tests.helpers import assert_close, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def setup():
+    cfg = W.custom_config("engine", hq=8, hkv=2, pre_chunks=((0, 200), (200, 180)), dec_batch=6,
+                          dec_len_lo=100, dec_len_hi=900)
+    wl = W.make_workload(cfg, seed=11)
+    dw = DeviceWorkload(wl)
+    eng = Engine([64, 128])
+    dec, pre = dw.engine_args()
+    yield wl, dw, eng, dec, pre
+    eng.close()
+    dw.close()
+
+
+def _plain_outputs(dw, eng, dec, pre):
+    """One decode and one prefill call on the whole device."""
+    ps, ds = eng.streams(-1)
+    mw.mw_decode_attn(dec["pool"], dw.hq, dw.hkv, dw.d, dw.scale, dw.dec_lens, dec["d_seq_lens"],
+                      dec["d_block_table"], dec["bt_stride"], dec["d_q"], dec["d_out"], dec["d_workspace"],
+                      dec["workspace_bytes"], 0, ds, None)
+    mw.mw_prefill_attn(pre["pool"], dw.hq, dw.hkv, dw.d, dw.scale, pre["new_lens"], pre["prefix_lens"],
+                       pre["d_qo_indptr"], pre["d_prefix_lens"], pre["d_block_table"], pre["bt_stride"],
+                       pre["d_q"], pre["d_out"], ps, None)
+    mw.mw_sync(ps)
+    mw.mw_sync(ds)
+    return dw.o_dec.clone(), dw.o_pre.clone()
+
+
+def test_engine_batch_of_chunks_matches_oracle(setup):
+    """The prefill batch the engine runs (every chunk in one call) and the
+    decode call agree with the oracle."""
+    wl, dw, eng, dec, pre = setup
+    say("engine: plain outputs vs oracle")
+    o_dec, o_pre = _plain_outputs(dw, eng, dec, pre)
+    c = wl.cfg
+    ref_pre = oracle.prefill(wl.q_pre[:c.pre_total], wl.k_pool, wl.v_pool, wl.pre_bt, 0)
+    assert_close(to_bits(o_pre[:c.pre_total]), ref_pre, "engine prefill batch")
+    ref_dec = oracle.decode(wl.q_dec, wl.k_pool, wl.v_pool, wl.dec_bt, wl.dec_lens)
+    assert_close(to_bits(o_dec), ref_dec, "engine decode")
+
+
+@pytest.mark.parametrize("policy,npl,switch", [
+    (mw.MW_ENGINE_BLOCKING, 24, False),
+    (mw.MW_ENGINE_POLLED, 3, False),
+    (mw.MW_ENGINE_POLLED, 3, True),
+    (mw.MW_ENGINE_POLLED, 1, True),
+])
+@pytest.mark.parametrize("config", [0, 1])
+def test_engine_runs_leave_outputs_unchanged(setup, policy, npl, switch, config):
+    wl, dw, eng, dec, pre = setup
+    say(f"engine run: policy {policy} N_PL {npl} switch {switch} partition {config}")
+    ref_dec, ref_pre = _plain_outputs(dw, eng, dec, pre)
+    dw.o_dec.zero_()
+    dw.o_pre.zero_()
+    torch.cuda.synchronize()
+    iters, layers, pl = 3, 4, 24
+    s = eng.run(dec, pre, config=config, decode_iters=iters, decode_layers=layers, prefill_layers=pl,
+                layers_per_launch=npl, policy=policy, switch_on_decode_end=switch)
+    assert torch.equal(dw.o_dec, ref_dec) and torch.equal(dw.o_pre, ref_pre)
+    td, tpf = mw.mw_engine_timeline(eng.h, 0), mw.mw_engine_timeline(eng.h, 1)
+    assert td.shape == (iters * layers, 3) and tpf.shape == (pl, 3)
+    for tl in (td, tpf):                 # calls of one stream: in order, no overlap
+        assert np.all(tl[:, 1] >= tl[:, 0]) and np.all(tl[1:, 0] >= tl[:-1, 1] - 1e-3)
+    assert abs((td[:, 1] - td[:, 0]).sum() - s["decode_busy_ms"]) < 1e-3
+    assert abs((tpf[:, 1] - tpf[:, 0]).sum() - s["prefill_busy_ms"]) < 1e-3
+    assert int(tpf[:, 2].sum()) == s["switched_layers"]
+    assert 0.0 <= s["decode_bubble"] < 1.0 and 0.0 <= s["prefill_bubble"] < 1.0
+    assert s["bubble_ratio"] == pytest.approx(0.5 * (s["decode_bubble"] + s["prefill_bubble"]))
+    assert 0.0 < s["decode_busy_ms"] <= s["wall_ms"] + 1e-6
+    assert 0.0 < s["prefill_busy_ms"] <= s["wall_ms"] + 1e-6
+    assert s["prefill_end_ms"] <= s["wall_ms"] + 1e-6
+    assert s["decode_iter_ms_mean"] > 0.0 and s["decode_gap_ms_max"] >= 0.0
+    if policy == mw.MW_ENGINE_BLOCKING:
+        assert s["prefill_batches"] == 1 and s["switched_layers"] == 0
+    else:
+        assert s["prefill_batches"] >= -(-pl // npl)
+        assert 0 <= s["switched_layers"] <= pl
+        if not switch:
+            assert s["switched_layers"] == 0 and s["switch_gap_ms"] == -1.0
+        elif s["switched_layers"] > 0:
+            assert s["switch_host_us"] >= 0.0
+
+
+def test_engine_switch_moves_late_layers_to_the_whole_device(setup):
+    """One short decode iteration and a long prefill: with N_PL = 1 almost
+    every prefill layer is still unlaunched when decode ends, so they move."""
+    wl, dw, eng, dec, pre = setup
+    say("engine switch")
+    s = eng.run(dec, pre, config=0, decode_iters=1, decode_layers=1, prefill_layers=64,
+                layers_per_launch=1, policy=mw.MW_ENGINE_POLLED, switch_on_decode_end=True)
+    assert s["switched_layers"] > 0
+    assert s["switch_gap_ms"] >= 0.0 and s["switch_host_us"] >= 0.0
+    assert s["prefill_batches"] == 64
+
+
+def test_engine_group_memory_and_streams(setup):
+    wl, dw, eng, dec, pre = setup
+    nbytes, ms = eng.memory()
+    assert ms > 0.0 and nbytes >= 0
+    p0, d0 = eng.streams(0)
+    p1, d1 = eng.streams(1)
+    pw, dwh = eng.streams(-1)
+    assert len({p0, d0, p1, d1}) == 4 and pw == dwh
+    with pytest.raises(mw.MWError):
+        eng.streams(2)
+    with pytest.raises(mw.MWError):
+        eng.run(dec, pre, config=2, decode_iters=1, decode_layers=1, prefill_layers=1, layers_per_launch=1)
+    with pytest.raises(mw.MWError):
+        eng.run(dec, pre, config=0, decode_iters=0, decode_layers=1, prefill_layers=1, layers_per_launch=1)
+
+
+def test_engine_rejects_bad_partitions():
+    for cus in ([0], [60], [256], [-8]):
+        with pytest.raises(mw.MWError):
+            Engine(cus)
