@@ -354,6 +354,16 @@ mw_status mw_prefill_layers(double t_decode_ms, double t_prefill_ms, int32_t n_l
  *     plan->switch_on_decode_end the layers launched after the last decode
  *     iteration ends go to the whole-device stream (ordered after the
  *     earlier layers by a cross-stream event wait).
+ *   plan->decode_graph = 1: a decode iteration is launched as one HIP graph
+ *     (paper Sec. 3.2: graphs for the decode phase only, one per batch size
+ *     and partition).  The engine captures it on the partition's decode
+ *     stream at the first run with these decode arguments, lengths, layer
+ *     count and partition, keeps it until mw_engine_destroy, and replays it
+ *     on later runs; the capture is outside the timed run.  The graph holds
+ *     the device pointers and lengths it was captured with: a caller that
+ *     changes the buffers' contents gets them read again, one that changes a
+ *     pointer or a length gets a new graph.  Stats then time each iteration
+ *     as one span.
  * Stats (device times from HIP events around every call, in ms from the
  * first launch): each stream's busy time (sum of its calls) and bubble ratio
  * (1 - busy / its first-start-to-last-end window), their mean, the longest
@@ -397,6 +407,7 @@ typedef struct {
     int32_t layers_per_launch;  /* N_PL, >= 1 (polled policy) */
     int32_t policy;             /* MW_ENGINE_BLOCKING or MW_ENGINE_POLLED */
     int32_t switch_on_decode_end;
+    int32_t decode_graph;       /* 1: each decode iteration is one graph launch */
 } mw_engine_plan;
 typedef struct {
     double wall_ms;                       /* first launch to last completion */
@@ -408,6 +419,7 @@ typedef struct {
     double switch_gap_ms;                 /* prefill timeline gap at the switch; -1 if none */
     double switch_host_us;                /* host time of the switch; -1 if none */
     double host_launch_ms;                /* host time spent launching */
+    double decode_launch_us_mean;         /* host time to launch one decode iteration */
     int32_t prefill_batches;              /* launch decisions that launched prefill layers */
     int32_t switched_layers;              /* prefill layers run on the whole device */
 } mw_engine_stats;
@@ -417,6 +429,12 @@ mw_status mw_engine_streams(const mw_engine *eng, int32_t config, mw_stream *pre
 mw_status mw_engine_memory(const mw_engine *eng, int64_t *device_bytes, double *create_ms);
 mw_status mw_engine_run(mw_engine *eng, const mw_decode_args *dec, const mw_prefill_args *pre,
                         const mw_engine_plan *plan, mw_engine_stats *stats);
+
+/* Captured decode graphs of `eng`: their count, the device memory their
+ * instantiation and upload took (free memory before minus after, summed)
+ * and the host time of capture + instantiation + upload.  Outputs may be
+ * NULL. */
+mw_status mw_engine_graphs(const mw_engine *eng, int32_t *n_graphs, int64_t *device_bytes, double *capture_ms);
 
 /* Per-call timeline of the last mw_engine_run on `eng`: phase 0 = decode
  * calls, 1 = prefill calls, in launch order.  Writes min(n_calls, capacity)

@@ -8,6 +8,7 @@
 
 #include <algorithm>
 #include <chrono>
+#include <cstring>
 #include <new>
 #include <vector>
 
@@ -25,6 +26,17 @@ struct mw_engine {
     double create_ms;
     // the last run's calls: (start ms, end ms, 1 if on the whole device)
     std::vector<double> timeline[2];
+    // captured decode iterations, one per (partition, decode arguments,
+    // lengths, layer count)
+    struct Graph {
+        int config, layers;
+        std::vector<unsigned char> key;
+        hipGraph_t graph;
+        hipGraphExec_t exec;
+        int64_t bytes;
+        double capture_ms;
+    };
+    std::vector<Graph> graphs;
 };
 
 namespace {
@@ -37,6 +49,14 @@ mw_status masked_stream(int n_words, const uint32_t *mask, hipStream_t *s) {
     const hipError_t e = hipExtStreamCreateWithCUMask(s, static_cast<uint32_t>(n_words), mask);
     if (e != hipSuccess) return fail(MW_ERR_HIP, "hipExtStreamCreateWithCUMask failed: %s", hipGetErrorString(e));
     return MW_OK;
+}
+
+void destroy_graphs(mw_engine *e) {
+    for (mw_engine::Graph &g : e->graphs) {
+        (void)hipGraphExecDestroy(g.exec);
+        (void)hipGraphDestroy(g.graph);
+    }
+    e->graphs.clear();
 }
 
 void destroy_streams(mw_engine *e) {
@@ -78,7 +98,23 @@ mw_status check_args(const mw_engine *eng, const mw_decode_args *dec, const mw_p
         return fail(MW_ERR_INVALID_ARG, "mw_engine_run: iteration and layer counts must be >= 1");
     if (pl->policy != MW_ENGINE_BLOCKING && pl->policy != MW_ENGINE_POLLED)
         return fail(MW_ERR_INVALID_ARG, "mw_engine_run: unknown policy %d", pl->policy);
+    if (pl->decode_graph != 0 && pl->decode_graph != 1)
+        return fail(MW_ERR_INVALID_ARG, "mw_engine_run: decode_graph must be 0 or 1");
+    if (pl->decode_graph && dec->batch > (1 << 20))
+        return fail(MW_ERR_INVALID_ARG, "mw_engine_run: decode batch too large");
     return MW_OK;
+}
+
+std::vector<unsigned char> graph_key(const mw_decode_args *dec, int layers) {
+    std::vector<unsigned char> k(sizeof(mw_decode_args) + sizeof(int) +
+                                 sizeof(int32_t) * static_cast<size_t>(std::max(dec->batch, 0)));
+    mw_decode_args a = *dec;
+    a.h_seq_lens = nullptr;     // the lengths' values matter, not where the host keeps them
+    std::memcpy(k.data(), &a, sizeof a);
+    std::memcpy(k.data() + sizeof a, &layers, sizeof layers);
+    if (dec->batch > 0 && dec->h_seq_lens)
+        std::memcpy(k.data() + sizeof a + sizeof layers, dec->h_seq_lens, sizeof(int32_t) * dec->batch);
+    return k;
 }
 
 }  // namespace
@@ -150,6 +186,7 @@ mw_status mw_engine_destroy(mw_engine *eng) {
     }
     const hipError_t c = hipStreamSynchronize(eng->whole);
     if (err == hipSuccess) err = c;
+    destroy_graphs(eng);
     destroy_streams(eng);
     delete eng;
     if (err != hipSuccess) return fail(MW_ERR_HIP, "mw_engine_destroy: %s", hipGetErrorString(err));
@@ -184,9 +221,49 @@ mw_status mw_engine_run(mw_engine *eng, const mw_decode_args *dec, const mw_pref
     MW_HIP_TRY(hipStreamSynchronize(ps));
     MW_HIP_TRY(hipStreamSynchronize(eng->whole));
 
+    // a decode iteration as one graph launch: looked up or captured (on the
+    // partition's decode stream) before anything is timed
+    hipGraphExec_t dgraph = nullptr;
+    if (plan->decode_graph) {
+        std::vector<unsigned char> key = graph_key(dec, plan->decode_layers);
+        for (const mw_engine::Graph &g : eng->graphs)
+            if (g.config == cfg && g.layers == plan->decode_layers && g.key == key) dgraph = g.exec;
+        if (!dgraph) {
+            mw_engine::Graph g{cfg, plan->decode_layers, key, nullptr, nullptr, 0, 0.0};
+            size_t f0 = 0, f1 = 0, tot = 0;
+            MW_HIP_TRY(hipDeviceSynchronize());
+            MW_HIP_TRY(hipMemGetInfo(&f0, &tot));
+            const clk::time_point t0 = clk::now();
+            MW_HIP_TRY(hipStreamBeginCapture(ds, hipStreamCaptureModeThreadLocal));
+            for (int l = 0; l < plan->decode_layers && st == MW_OK; ++l)
+                st = mw_decode_attn(dec->pool, &dec->shape, dec->batch, dec->h_seq_lens, dec->d_seq_lens,
+                                    dec->d_block_table, dec->bt_stride, dec->d_q, dec->d_out, dec->d_workspace,
+                                    dec->workspace_bytes, dec->chunk_pages, ds, nullptr);
+            const hipError_t ec = hipStreamEndCapture(ds, &g.graph);
+            if (st == MW_OK && ec != hipSuccess)
+                st = fail(MW_ERR_HIP, "hipStreamEndCapture failed: %s", hipGetErrorString(ec));
+            if (st == MW_OK && hipGraphInstantiate(&g.exec, g.graph, nullptr, nullptr, 0) != hipSuccess)
+                st = fail(MW_ERR_HIP, "hipGraphInstantiate failed");
+            if (st == MW_OK && hipGraphUpload(g.exec, ds) != hipSuccess) st = fail(MW_ERR_HIP, "hipGraphUpload failed");
+            if (st == MW_OK && hipStreamSynchronize(ds) != hipSuccess) st = fail(MW_ERR_HIP, "graph upload failed");
+            if (st != MW_OK) {
+                if (g.exec) (void)hipGraphExecDestroy(g.exec);
+                if (g.graph) (void)hipGraphDestroy(g.graph);
+                (void)hipGetLastError();
+                (void)hipSetDevice(prev);
+                return st;
+            }
+            g.capture_ms = ms_since(t0);
+            if (hipMemGetInfo(&f1, &tot) == hipSuccess) g.bytes = static_cast<int64_t>(f0) - static_cast<int64_t>(f1);
+            eng->graphs.push_back(g);
+            dgraph = g.exec;
+        }
+    }
+    const int calls_per_iter = dgraph ? 1 : plan->decode_layers;
+
     // all events up front: creating one inside the loop would add host time there
     EventPool pool;
-    const size_t n_events = 1 + 2 * (static_cast<size_t>(plan->decode_iters) * plan->decode_layers +
+    const size_t n_events = 1 + 2 * (static_cast<size_t>(plan->decode_iters) * calls_per_iter +
                                      static_cast<size_t>(plan->prefill_layers));
     for (size_t i = 0; i < n_events && st == MW_OK; ++i) {
         hipEvent_t e;
@@ -205,7 +282,7 @@ mw_status mw_engine_run(mw_engine *eng, const mw_decode_args *dec, const mw_pref
     std::vector<Span> dspan, pspan;     // per call
     std::vector<int> pstream;           // per prefill call: 0 = partition, 1 = whole device
     std::vector<hipEvent_t> iter_end;   // per decode iteration
-    double host_ms = 0.0;
+    double host_ms = 0.0, dec_host_ms = 0.0;
     int prefill_batches = 0, switched = 0;
     double switch_host_us = -1.0;
     int switch_at = -1;                 // first prefill call on the whole device
@@ -232,14 +309,20 @@ mw_status mw_engine_run(mw_engine *eng, const mw_decode_args *dec, const mw_pref
                                pre->d_qo_indptr, pre->d_prefix_lens, pre->d_block_table, pre->bt_stride, pre->d_q,
                                pre->d_out, s, nullptr);
     };
+    auto graph_call = [&](hipStream_t s) -> mw_status {
+        MW_HIP_TRY(hipGraphLaunch(dgraph, s));
+        return MW_OK;
+    };
     auto launch_iteration = [&]() -> mw_status {
         const clk::time_point t0 = clk::now();
-        for (int l = 0; l < plan->decode_layers; ++l) {
-            mw_status r = span_around(ds, dspan, decode_call);
+        for (int l = 0; l < calls_per_iter; ++l) {
+            mw_status r = dgraph ? span_around(ds, dspan, graph_call) : span_around(ds, dspan, decode_call);
             if (r != MW_OK) return r;
         }
         iter_end.push_back(dspan.back().end);
-        host_ms += ms_since(t0);
+        const double dt = ms_since(t0);
+        host_ms += dt;
+        dec_host_ms += dt;
         return MW_OK;
     };
     hipStream_t pcur = ps;
@@ -339,7 +422,7 @@ mw_status mw_engine_run(mw_engine *eng, const mw_decode_args *dec, const mw_pref
     mw_engine_stats s{};
     // decode stream
     double busy = 0.0, first = 1e30, last = 0.0, gap_max = 0.0, iter_sum = 0.0;
-    const int L = plan->decode_layers;
+    const size_t L = static_cast<size_t>(calls_per_iter);
     for (size_t i = 0; i < dspan.size(); ++i) {
         const double a = at(dspan[i].start), b = at(dspan[i].end);
         busy += b - a;
@@ -376,6 +459,7 @@ mw_status mw_engine_run(mw_engine *eng, const mw_decode_args *dec, const mw_pref
     s.switch_gap_ms = switch_at > 0 ? at(pspan[switch_at].start) - at(pspan[switch_at - 1].end) : -1.0;
     s.switch_host_us = switch_host_us;
     s.host_launch_ms = host_ms;
+    s.decode_launch_us_mean = 1e3 * dec_host_ms / static_cast<double>(iter_end.size());
     s.prefill_batches = prefill_batches;
     s.switched_layers = switched;
     *stats = s;
@@ -390,6 +474,20 @@ mw_status mw_engine_run(mw_engine *eng, const mw_decode_args *dec, const mw_pref
         }
     }
     (void)hipSetDevice(prev);
+    return MW_OK;
+}
+
+mw_status mw_engine_graphs(const mw_engine *eng, int32_t *n_graphs, int64_t *device_bytes, double *capture_ms) {
+    if (!eng) return fail(MW_ERR_INVALID_ARG, "mw_engine_graphs: NULL engine");
+    int64_t b = 0;
+    double ms = 0.0;
+    for (const mw_engine::Graph &g : eng->graphs) {
+        b += g.bytes;
+        ms += g.capture_ms;
+    }
+    if (n_graphs) *n_graphs = static_cast<int32_t>(eng->graphs.size());
+    if (device_bytes) *device_bytes = b;
+    if (capture_ms) *capture_ms = ms;
     return MW_OK;
 }
 

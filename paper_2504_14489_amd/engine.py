@@ -43,10 +43,17 @@ class Engine:
 
     def run(self, dec: dict, pre: dict, *, config: int = 0, decode_iters: int, decode_layers: int,
             prefill_layers: int, layers_per_launch: int, policy: int = mw.MW_ENGINE_POLLED,
-            switch_on_decode_end: bool = True) -> dict:
+            switch_on_decode_end: bool = True, decode_graph: bool = False) -> dict:
         plan = mw.EnginePlan(config, decode_iters, decode_layers, prefill_layers, layers_per_launch,
-                             policy, int(switch_on_decode_end))
+                             policy, int(switch_on_decode_end), int(decode_graph))
         return mw.mw_engine_run(self.h, dec, pre, plan)
+
+    def graphs(self):
+        """(captured decode graphs, their device bytes, capture ms)."""
+        return mw.mw_engine_graphs(self.h)
+
+    def timeline(self, phase: int):
+        return mw.mw_engine_timeline(self.h, phase)
 
     def close(self):
         if self.h is not None:
@@ -78,6 +85,12 @@ VARIANTS = {
     "polled_layer1": lambda n_pl, p: dict(policy=mw.MW_ENGINE_POLLED, layers_per_launch=1,
                                           switch_on_decode_end=False),
     "polled_all": lambda n_pl, p: dict(policy=mw.MW_ENGINE_POLLED, layers_per_launch=p, switch_on_decode_end=False),
+    "polled_graph": lambda n_pl, p: dict(policy=mw.MW_ENGINE_POLLED, layers_per_launch=n_pl,
+                                         switch_on_decode_end=False, decode_graph=True),
+    "polled_switch_graph": lambda n_pl, p: dict(policy=mw.MW_ENGINE_POLLED, layers_per_launch=n_pl,
+                                                switch_on_decode_end=True, decode_graph=True),
+    "blocking_graph": lambda n_pl, p: dict(policy=mw.MW_ENGINE_BLOCKING, layers_per_launch=p,
+                                           switch_on_decode_end=False, decode_graph=True),
 }
 
 
@@ -92,10 +105,46 @@ def scenarios(L: int, args) -> Dict:
         paper's second bubble, removed by the switch)."""
     return {
         "steady": (L, args.decode_iters, L * args.prefill_batches,
-                   ["blocking", "polled", "polled_switch", "polled_layer1", "polled_all"]),
-        "launch_bound": (2, 4 * args.decode_iters, L * args.prefill_batches, ["blocking", "polled"]),
-        "decode_ends": (L, 2, 2 * L * args.prefill_batches, ["polled", "polled_switch"]),
+                   ["blocking", "polled", "polled_switch", "polled_layer1", "polled_all", "polled_graph"]),
+        "launch_bound": (2, 4 * args.decode_iters, L * args.prefill_batches,
+                         ["blocking", "polled", "blocking_graph", "polled_graph"]),
+        "decode_ends": (L, 2, 2 * L * args.prefill_batches, ["polled", "polled_switch", "polled_switch_graph"]),
     }
+
+
+def write_table(out: Dict, path: str, argv):
+    """Markdown summary of one measurement (the numbers the design notes use)."""
+    cmd = "python -m paper_2504_14489_amd.engine " + " ".join(argv)
+    g, dg = out["group"], out.get("decode_graphs", {})
+    lines = [f"# Multiplex engine, workload {out['workload']} (N_T = {out['model_layers']} calls per decode iteration)",
+             "", f"Command: `{cmd}`", "",
+             f"Partition group: {g['partitions']} partition(s) + whole-device stream, "
+             f"{g['device_bytes'] / 2**20:.2f} MiB device memory, created in {g['create_ms']:.2f} ms.",
+             f"Decode graphs: {dg.get('graphs', 0)}, {dg.get('device_bytes', 0) / 2**20:.2f} MiB, "
+             f"{dg.get('capture_ms', 0.0):.2f} ms to capture, instantiate and upload.", ""]
+    for p in out["partitions"]:
+        lines += [f"## Prefill on {p['prefill_cus']} CUs (solo: decode call {p['decode_layer_ms']:.3f} ms, "
+                  f"prefill call {p['prefill_layer_ms']:.3f} ms)", "",
+                  f"Layer-wise launch overhead on the prefill end, steady scenario: N_PL from the formula "
+                  f"{100 * p['layerwise_overhead_npl']:+.2f}%, one layer per launch "
+                  f"{100 * p['layerwise_overhead']:+.2f}% (both against the whole job in one launch).", "",
+                  "| scenario | variant | N_PL | wall ms | bubble % (decode / prefill) | decode iteration ms | "
+                  "iteration gap us (median / max) | decode launch us | prefill end ms | switched layers | "
+                  "switch: GPU gap / host us |", "|---|---|---|---|---|---|---|---|---|---|---|"]
+        for sc_name, sc in p["scenarios"].items():
+            for name, r in sc["runs"].items():
+                sw = (f"{1e3 * r['switch_gap_ms']:.1f} / {r['switch_host_us']:.1f}"
+                      if r["switch_gap_ms"] >= 0 else "-")
+                lines.append(
+                    f"| {sc_name} ({sc['decode_iters']} x {sc['decode_layers']} decode, {sc['prefill_layers']} prefill) "
+                    f"| {name} | {r['n_pl_used']:.0f} | {r['wall_ms']:.2f} | {100 * r['bubble_ratio']:.2f} "
+                    f"({100 * r['decode_bubble']:.2f} / {100 * r['prefill_bubble']:.2f}) | "
+                    f"{r['decode_iter_ms_mean']:.3f} | {1e3 * r['iter_gap_ms_median']:.1f} / "
+                    f"{1e3 * r['iter_gap_ms_max']:.1f} | {r['decode_launch_us_mean']:.0f} | {r['prefill_end_ms']:.2f} | "
+                    f"{r['switched_layers']:.0f} | {sw} |")
+        lines.append("")
+    with open(path, "w") as f:
+        f.write("\n".join(lines))
 
 
 def main(argv=None):
@@ -112,6 +161,8 @@ def main(argv=None):
                     help="prefill jobs of N_T layers each, run back to back")
     ap.add_argument("--reps", type=int, default=3)
     ap.add_argument("--out", default="")
+    ap.add_argument("--table", default="", help="also write a Markdown summary here")
+    argv = sys.argv[1:] if argv is None else list(argv)
     args = ap.parse_args(argv)
 
     cfg = W.CONFIGS[args.config]
@@ -173,8 +224,9 @@ def main(argv=None):
                     runs = [eng.run(dec, pre, **plan) for _ in range(args.reps)]
                     same = bool(torch.equal(ref_dec, dw.o_dec) and torch.equal(ref_pre, dw.o_pre))
                     st = _median_stats(runs)
-                    st.update(gap_stats(mw.mw_engine_timeline(eng.h, 0), d_layers))
+                    st.update(gap_stats(eng.timeline(0), 1 if v.get("decode_graph") else d_layers))
                     st["outputs_equal_reference"] = same
+                    st["n_pl_used"] = v["layers_per_launch"]
                     sc["runs"][name] = st
                     log(f"[engine] {p_cus:3d} CUs {sc_name:10s} {name:14s} wall {st['wall_ms']:7.2f} ms, "
                         f"bubble {100 * st['bubble_ratio']:5.2f}% (decode {100 * st['decode_bubble']:5.2f}%, "
@@ -182,7 +234,8 @@ def main(argv=None):
                         f"iteration gap med/max {1e3 * st['iter_gap_ms_median']:.1f}/"
                         f"{1e3 * st['iter_gap_ms_max']:.1f} us, call gap med {1e3 * st['call_gap_ms_median']:.1f} us, "
                         f"prefill end {st['prefill_end_ms']:.2f} ms, switched {st['switched_layers']:.0f}, "
-                        f"N_PL {v['layers_per_launch']}, same {same}")
+                        f"N_PL {v['layers_per_launch']}, host launch {st['host_launch_ms']:.2f} ms "
+                        f"(decode iteration {st['decode_launch_us_mean']:.0f} us), same {same}")
                     if not same:
                         raise SystemExit("engine outputs differ from the reference call")
                 part["scenarios"][sc_name] = sc
@@ -190,6 +243,9 @@ def main(argv=None):
             part["layerwise_overhead"] = r["polled_layer1"]["prefill_end_ms"] / r["polled_all"]["prefill_end_ms"] - 1
             part["layerwise_overhead_npl"] = r["polled"]["prefill_end_ms"] / r["polled_all"]["prefill_end_ms"] - 1
             out["partitions"].append(part)
+        n_g, g_bytes, g_ms = eng.graphs()
+        out["decode_graphs"] = {"graphs": n_g, "device_bytes": g_bytes, "capture_ms": g_ms}
+        log(f"[engine] {n_g} decode graphs: {g_bytes / 2**20:.2f} MiB, {g_ms:.1f} ms to capture")
     finally:
         eng.close()
         dw.close()
@@ -198,6 +254,8 @@ def main(argv=None):
     if args.out:
         with open(args.out, "w") as f:
             f.write(line + "\n")
+    if args.table:
+        write_table(out, args.table, argv)
 
 
 if __name__ == "__main__":

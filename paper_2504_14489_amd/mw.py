@@ -74,14 +74,14 @@ class EnginePlan(ctypes.Structure):
     _fields_ = [("config", ctypes.c_int32), ("decode_iters", ctypes.c_int32),
                 ("decode_layers", ctypes.c_int32), ("prefill_layers", ctypes.c_int32),
                 ("layers_per_launch", ctypes.c_int32), ("policy", ctypes.c_int32),
-                ("switch_on_decode_end", ctypes.c_int32)]
+                ("switch_on_decode_end", ctypes.c_int32), ("decode_graph", ctypes.c_int32)]
 
 
 class EngineStats(ctypes.Structure):
     _fields_ = [(f, ctypes.c_double) for f in (
         "wall_ms", "decode_busy_ms", "prefill_busy_ms", "decode_bubble", "prefill_bubble", "bubble_ratio",
         "decode_gap_ms_max", "decode_iter_ms_mean", "prefill_end_ms", "switch_gap_ms", "switch_host_us",
-        "host_launch_ms")] + [("prefill_batches", ctypes.c_int32), ("switched_layers", ctypes.c_int32)]
+        "host_launch_ms", "decode_launch_us_mean")] + [("prefill_batches", ctypes.c_int32), ("switched_layers", ctypes.c_int32)]
 
     def as_dict(self) -> dict:
         return {f: getattr(self, f) for f, _ in self._fields_}
@@ -150,6 +150,7 @@ _SIGNATURES = {
     "mw_engine_run": ([_P, ctypes.POINTER(_DecodeArgs), ctypes.POINTER(_PrefillArgs),
                        ctypes.POINTER(EnginePlan), ctypes.POINTER(EngineStats)], _I),
     "mw_engine_timeline": ([_P, _I, _PD, _I, _PI], _I),
+    "mw_engine_graphs": ([_P, _PI, ctypes.POINTER(ctypes.c_int64), _PD], _I),
 }
 
 EXPORTED = tuple(_SIGNATURES)
@@ -506,3 +507,10 @@ def mw_engine_timeline(eng, phase: int) -> np.ndarray:
     if n.value:
         _check(load().mw_engine_timeline(eng, phase, out.ctypes.data_as(_PD), n.value, ctypes.byref(n)))
     return out
+
+
+def mw_engine_graphs(eng) -> Tuple[int, int, float]:
+    """(number of captured decode graphs, their device bytes, capture ms)."""
+    n, b, ms = ctypes.c_int32(), ctypes.c_int64(), ctypes.c_double()
+    _check(load().mw_engine_graphs(eng, ctypes.byref(n), ctypes.byref(b), ctypes.byref(ms)))
+    return n.value, b.value, ms.value

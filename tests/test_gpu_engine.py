@@ -129,3 +129,65 @@ def test_engine_rejects_bad_partitions():
     for cus in ([0], [60], [256], [-8]):
         with pytest.raises(mw.MWError):
             Engine(cus)
+
+
+def test_engine_decode_graph_replays_match_eager(setup):
+    """Decode iterations as graph launches: every replay recomputes the
+    outputs (zeroed before each run, eager calls in between) and one graph
+    serves every run with the same arguments and partition."""
+    wl, dw, eng, dec, pre = setup
+    say("engine decode graph replays")
+    ref_dec, ref_pre = _plain_outputs(dw, eng, dec, pre)
+    n0 = eng.graphs()[0]
+    for rep in range(4):
+        dw.o_dec.zero_()
+        dw.o_pre.zero_()
+        torch.cuda.synchronize()
+        s = eng.run(dec, pre, config=0, decode_iters=3, decode_layers=4, prefill_layers=12,
+                    layers_per_launch=3, policy=mw.MW_ENGINE_POLLED, switch_on_decode_end=True,
+                    decode_graph=True)
+        assert torch.equal(dw.o_dec, ref_dec), f"replay {rep}"
+        assert torch.equal(dw.o_pre, ref_pre), f"replay {rep}"
+        assert mw.mw_engine_timeline(eng.h, 0).shape == (3, 3)      # one span per iteration
+        assert s["decode_iter_ms_mean"] > 0.0
+        _plain_outputs(dw, eng, dec, pre)                            # eager work between replays
+    n1, nbytes, ms = eng.graphs()
+    assert n1 == n0 + 1 and nbytes >= 0 and ms > 0.0
+    eng.run(dec, pre, config=1, decode_iters=1, decode_layers=4, prefill_layers=2, layers_per_launch=1,
+            decode_graph=True)
+    eng.run(dec, pre, config=0, decode_iters=1, decode_layers=2, prefill_layers=2, layers_per_launch=1,
+            decode_graph=True)
+    assert eng.graphs()[0] == n0 + 3                                  # per partition and layer count
+    assert torch.equal(dw.o_dec, ref_dec)
+
+
+def test_graph_launched_on_a_partition_stream_keeps_its_cus():
+    """A graph replayed on a CU-masked stream runs its kernels on that
+    stream's CUs only (what per-partition decode graphs rely on)."""
+    from paper_2504_14489_amd.device import Partition
+    from tests.test_gpu_partition import cu_ids
+    say("graph on a masked stream")
+    part = Partition(64, 192)
+    n_blocks = 2048
+    eager = torch.zeros(4 * n_blocks, dtype=torch.int32, device="cuda:0")
+    graphed = torch.zeros_like(eager)
+    torch.cuda.synchronize()
+    try:
+        mw.mw_cu_probe(n_blocks, 20000, eager.data_ptr(), part.decode_stream)
+        mw.mw_sync(part.decode_stream)
+        ext = torch.cuda.ExternalStream(part.decode_stream)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=ext):
+            mw.mw_cu_probe(n_blocks, 20000, graphed.data_ptr(), part.decode_stream)
+        for _ in range(2):
+            graphed.zero_()
+            torch.cuda.synchronize()
+            with torch.cuda.stream(ext):
+                g.replay()
+            torch.cuda.synchronize()
+            got = {tuple(x) for x in cu_ids(graphed.cpu().numpy().astype(np.uint32).reshape(-1, 4))}
+            want = {tuple(x) for x in cu_ids(eager.cpu().numpy().astype(np.uint32).reshape(-1, 4))}
+            assert len(want) == 192 and got <= want, f"{len(got - want)} CUs outside the partition"
+        del g
+    finally:
+        part.close()
