@@ -183,6 +183,56 @@ class Bench:
         return {"wall_s": wall, "prefill_k": pre_k, "decode_k0": dec_k0, "decode_call": dec_call,
                 "prefill_window_ms": [p_start, p_stop], "decode_window_ms": [0.0, d_stop]}
 
+    # --------------------------------------------- temporal baselines --
+    def temporal(self, kind, steps, m):
+        """Wall ms per step of the same work without CU partitions, on the
+        whole GPU: "serial" = prefill, then m decode iterations, one stream;
+        "free" = the two phases on two unmasked streams (the hardware shares
+        the CUs); "fused" = appends, one fused prefill + decode launch, then
+        m - 1 more decode iterations."""
+        torch = self.torch
+        from paper_2504_14489_amd import mw
+        s1 = self.full.cuda_stream
+        if not hasattr(self, "full2"):
+            self.full2 = torch.cuda.Stream()
+            self.eng_dec, self.eng_pre = self.dw.engine_args()
+
+        td = []
+
+        def step(timed=False):
+            if kind == "serial":
+                self.prefill_call(s1)
+                for _ in range(m):
+                    self.decode_call(s1)
+            elif kind == "free":
+                s2 = self.full2.cuda_stream
+                for _ in range(m):
+                    t = self.Timing() if timed else None
+                    self.decode_call(s2, None, t)
+                    if t is not None:
+                        td.append(t)
+                self.prefill_call(s1)
+            else:
+                for (r, n), (k, v) in zip(self.chunks, self.pre_new):
+                    self.dw.write_prefill_kv(r, n, k, v, s1)
+                self.dw.write_decode_kv(self.dec_new[0], self.dec_new[1], s1)
+                mw.mw_fused_attn(self.eng_pre, self.eng_dec, s1)
+                for _ in range(m - 1):
+                    self.decode_call(s1)
+
+        for _ in range(max(1, self.args.warmup)):
+            step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            step(timed=True)
+        torch.cuda.synchronize()
+        ms = 1e3 * (time.perf_counter() - t0) / steps
+        # a decode token is ready when its iteration ends: on one stream that
+        # is the end of the step, next to the prefill it is the decode call
+        dec_ms = median([t.elapsed()[0] for t in td]) if td else ms / m
+        return ms, dec_ms
+
     def close(self):
         self.dw.close()
 
@@ -422,6 +472,20 @@ def main():
     for p_cus, d_cus in splits:
         results.append(run_partition(b, p_cus, d_cus, args))
     par = None if args.no_parity else parity(b)
+    # the paper's core comparison (spatial vs temporal or fused sharing) at
+    # equal work: the same step on the whole GPU without partitions
+    m = results[0]["decode_iters_per_step"]
+    res = {k: b.temporal(k, args.steps, m) for k in ("serial", "free", "fused")}
+    base = {k: v[0] for k, v in res.items()}
+    spatial = results[0]["ms_per_step"]
+    spatial_dec = results[0]["mux"]["decode_call_ms"]
+    baselines = {"spatial_ms_per_step": spatial, "serial_ms_per_step": base["serial"],
+                 "free_streams_ms_per_step": base["free"], "fused_ms_per_step": base["fused"],
+                 "spatial_speedup": {k: base[k] / spatial for k in base},
+                 "decode_iteration_ms": {"spatial": spatial_dec, **{k: v[1] for k, v in res.items()}}}
+    log(f"[bench] equal-work step: spatial {spatial:.3f} ms, serial {base['serial']:.3f}, "
+        f"free streams {base['free']:.3f}, fused {base['fused']:.3f}; decode iteration: spatial "
+        f"{spatial_dec:.3f}, serial {res['serial'][1]:.3f}, free {res['free'][1]:.3f}, fused {res['fused'][1]:.3f}")
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample ...")
@@ -461,6 +525,7 @@ def main():
         "roofline_other": other,
         "cpu_baseline": cpu,
         "partitions": results,
+        "temporal_baselines": baselines,
         "parity": par,
     }
     print(json.dumps(line), flush=True)

@@ -423,6 +423,19 @@ typedef struct {
     int32_t prefill_batches;              /* launch decisions that launched prefill layers */
     int32_t switched_layers;              /* prefill layers run on the whole device */
 } mw_engine_stats;
+/* One launch covering a prefill call and a decode call on the same pool: the
+ * fused comparator (paper Sec. 5: the chunked-prefill baseline runs prefill
+ * and decode attention in one kernel on the whole GPU).  Each work-group of
+ * the fused kernel is either one prefill work-group or two decode work
+ * units; the two kinds are interleaved in dispatch order in proportion to
+ * their counts, then the decode combine kernel runs.  Arguments, layouts and
+ * results are those of mw_prefill_attn (pre) and mw_decode_attn (dec) with
+ * the same checks; both must name the same pool, and the prefill outputs must
+ * not overlap the decode outputs or workspace.  Outputs are bit-identical to
+ * the two separate calls.  timing records 2 kernels (fused, combine). */
+mw_status mw_fused_attn(const mw_prefill_args *pre, const mw_decode_args *dec, mw_stream stream,
+                        mw_timing *timing);
+
 mw_status mw_engine_create(int32_t device, const int32_t *prefill_cus, int32_t n, mw_engine **out);
 mw_status mw_engine_destroy(mw_engine *eng);
 mw_status mw_engine_streams(const mw_engine *eng, int32_t config, mw_stream *prefill, mw_stream *decode);

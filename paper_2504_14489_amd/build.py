@@ -19,7 +19,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libmw.so")
 
-SOURCES = ["runtime.hip", "kv_pool.hip", "decode_attn.hip", "prefill_attn.hip", "estimator.cpp", "engine.cpp"]
+SOURCES = ["runtime.hip", "kv_pool.hip", "decode_attn.hip", "prefill_attn.hip", "fused_attn.hip", "estimator.cpp", "engine.cpp"]
 ARCH = "gfx950"
 # Packed FP32 instructions are disabled: hipcc would otherwise form
 # v_pk_{add,mul,fma}_f32 from ordinary float code.

@@ -1,0 +1,297 @@
+// Device body of the split-K decode attention (one work unit), shared by
+// the decode kernel and the fused prefill + decode kernel.
+//
+// Decode is memory-bound (paper Sec. 2.2: the decode phase is
+// memory-intensive; Sec. 3.3, Table "tab:theory_cost": O(d^2 + (r+1) d)), so
+// the design goal is streaming every K/V byte of the batch from HBM exactly
+// once with enough bytes in flight; arithmetic is kept off the vector ALU.
+//
+// Work-group = (sequence b, kv head, chunk of CH consecutive pages), 4 waves.
+// The split depends only on the sequence lengths (never on page ids), so a
+// result does not change when pages are renumbered.
+//
+// Each wave streams its own pages of the chunk two at a time (a "pair"), with
+// the next pair's loads in flight while the current pair is computed:
+//   * K rows are loaded straight into the A operand of a 16x16x32 bf16 MFMA
+//     (one page = 16 tokens x 32 dims per step), B = Q^T of the kv head's G
+//     query heads (columns >= G are zero): S^T[token][head].
+//   * V rows go to a per-wave LDS buffer as loaded (16-byte row-major stores)
+//     and come back through the transposing LDS read as the A operand of a
+//     second MFMA, O^T[d][head] += V^T[d][token] P^T[token][head]; P^T is the
+//     S^T accumulator itself, converted to bf16.
+//   * online softmax per pair in base 2; the reference maximum moves only
+//     when a column's maximum grows by more than 2^8 (O and l are then
+//     rescaled), which the result O / l does not depend on.
+// The 4 waves' (m, l, O) are merged in LDS at the end; a sequence that fits
+// one chunk writes its bf16 output directly, otherwise the chunk's partial goes
+// to the workspace and the combine kernel merges the chunks of each
+// (sequence, kv head) with the log-sum-exp identity
+//   M = max m_s,  O = sum 2^(m_s - M) o_s / sum 2^(m_s - M) l_s.
+#pragma once
+#include "mw_internal.h"
+
+namespace {
+namespace dk {
+
+using namespace mw;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kPair = 2;                      // pages per wave step
+constexpr int VSTR = 144;                     // LDS V row stride (bf16): conflict-free
+constexpr int kVBufElems = 16 * kPair * VSTR; // one wave's V buffer
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kRescaleLog2 = 8.f;
+// chunk_pages = 0: the largest of 128, 64, 32 pages that still gives at least
+// kAutoMinUnits work-groups (longer chunks amortise each work-group's set-up
+// and merge; enough work-groups keep every CU of a partition streaming)
+constexpr int kAutoChunks[3] = {128, 64, 32};
+constexpr int64_t kAutoMinUnits = 1024;
+
+__device__ inline uint16_t to_bf16(float f) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f)); }
+__device__ inline uint32_t cvt2(float a, float b) {
+    bf16x2 v;
+    v[0] = static_cast<__bf16>(a);
+    v[1] = static_cast<__bf16>(b);
+    return __builtin_bit_cast(uint32_t, v);
+}
+__device__ inline uint4 sel4(bool ok, uint4 v) {
+    return make_uint4(ok ? v.x : 0u, ok ? v.y : 0u, ok ? v.z : 0u, ok ? v.w : 0u);
+}
+__device__ inline i16x4 lds_read_tr(const uint16_t *p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        reinterpret_cast<__attribute__((address_space(3))) i16x4 *>(reinterpret_cast<uintptr_t>(p)));
+}
+
+__device__ inline int chunks_of(int L, int ch_pages, int bt_stride) {
+    if (L <= 0) return 0;
+    int np = (L + kPageSize - 1) / kPageSize;
+    np = np < bt_stride ? np : bt_stride;
+    return (np + ch_pages - 1) / ch_pages;
+}
+
+// Wave-level search for the sequence b and chunk c holding global chunk ci
+// (every wave runs it; no barrier).  Returns false if ci is past the end.
+__device__ bool locate_chunk(const int32_t *__restrict__ seq_lens, int batch, int ch_pages, int bt_stride,
+                             int ci, int &b_out, int &c_out, int &nch_out, int &first_out) {
+    const int lane = threadIdx.x & 63;
+    int running = 0;
+    for (int base = 0; base < batch; base += 64) {
+        const int bb = base + lane;
+        const int n = bb < batch ? chunks_of(seq_lens[bb], ch_pages, bt_stride) : 0;
+        int x = n;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int y = __shfl_up(x, off);
+            if (lane >= off) x += y;
+        }
+        const int incl = running + x, excl = incl - n;
+        const uint64_t hit = __builtin_amdgcn_ballot_w64(bb < batch && ci >= excl && ci < incl);
+        if (hit) {
+            const int src = __builtin_ctzll(hit);
+            first_out = __shfl(excl, src);
+            b_out = base + src;
+            c_out = ci - first_out;
+            nch_out = __shfl(n, src);
+            return true;
+        }
+        running = __shfl(incl, 63);
+    }
+    return false;
+}
+
+struct PairRegs {
+    uint4 k[kPair][4];  // K rows as the MFMA A operand: token = lane%16, dims 32kb + 8(lane/16) + 0..7
+    uint4 v[kPair][4];  // V rows: token 4i + lane/16, dims 8(lane%16) + 0..7
+    bool ok[kPair];
+};
+
+__device__ inline void pair_load(PairRegs &pr, const uint16_t *__restrict__ kpool,
+                                 const uint16_t *__restrict__ vpool, const int32_t *__restrict__ btrow,
+                                 int p0, int p_end, int hkv, int kvh, int num_pages) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int j = 0; j < kPair; ++j) {
+        const int p = p0 + j;
+        const int page = btrow[p < p_end ? p : p0];
+        pr.ok[j] = p < p_end && page >= 0 && page < num_pages;
+        const size_t base = (static_cast<size_t>(pr.ok[j] ? page : 0) * hkv + kvh) * (kPageSize * kHeadDim);
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+            pr.k[j][kb] = *reinterpret_cast<const uint4 *>(kpool + base + (lane & 15) * kHeadDim + 32 * kb +
+                                                          8 * (lane >> 4));
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            pr.v[j][i] = *reinterpret_cast<const uint4 *>(vpool + base + (4 * i + (lane >> 4)) * kHeadDim +
+                                                         8 * (lane & 15));
+    }
+}
+
+// One (sequence, kv head, chunk) work unit on 4 waves.  tid = thread index
+// within the 4 waves (0..255); s_v, s_m, s_l are those waves' LDS.
+// kGuarded: the caller runs other work in the same work-group, so a unit
+// past the end does nothing but still takes the two work-group barriers.
+template <bool kGuarded>
+__device__ __forceinline__ void
+decode_unit(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpool,
+               const uint16_t *__restrict__ q, uint16_t *__restrict__ out,
+               const int32_t *__restrict__ seq_lens, const int32_t *__restrict__ bt, int bt_stride,
+               float *__restrict__ ws_o, float2 *__restrict__ ws_ml, int32_t *__restrict__ ws_cbase,
+               int batch, int hkv, int group, int num_pages, float scale_log2, int ch_pages,
+            int u, int tid, uint16_t *s_v, float (*s_m)[16], float (*s_l)[16]) {
+
+    const int kvh = u % hkv;
+    int b = 0, c = 0, nch = 0, first = 0;
+    const bool found = locate_chunk(seq_lens, batch, ch_pages, bt_stride, u / hkv, b, c, nch, first);
+    // more units than the device lengths give (uniform over the 4 waves): a
+    // kernel of its own returns; a fused work-group still takes both barriers
+    if constexpr (!kGuarded) {
+        if (!found) return;
+    }
+
+    const int lane = tid & 63, wave = tid >> 6;
+    const int col = lane & 15, grp = lane >> 4;
+    const int L = min(seq_lens[b], bt_stride * kPageSize);
+    const int np_b = (L + kPageSize - 1) / kPageSize;
+    const int p_end = found ? min((c + 1) * ch_pages, np_b) : 0;
+    const int32_t *btrow = bt + static_cast<size_t>(b) * bt_stride;
+    const int hq = hkv * group;
+
+    // Q^T operand: column `col` is query head kvh*group + col
+    uint4 qop[4];
+    {
+        const bool hv = col < group;
+        const uint16_t *qp = q + (static_cast<size_t>(b) * hq + kvh * group + (hv ? col : 0)) * kHeadDim + 8 * grp;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+            qop[kb] = hv ? *reinterpret_cast<const uint4 *>(qp + 32 * kb) : make_uint4(0, 0, 0, 0);
+    }
+
+    f32x4 oacc[8];  // O^T[d = 16db + 4grp + i][head = col]
+#pragma unroll
+    for (int db = 0; db < 8; ++db) oacc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m_run = -INFINITY, l_run = 0.f;
+
+    uint16_t *vbuf = s_v + wave * kVBufElems;
+    // transposing-read source: lane s of 16-lane group g -> row 4g + s/4 (+16 for
+    // the second page), dims 4(s%4) (+16 db)
+    const uint16_t *vtr = vbuf + (4 * grp + (col >> 2)) * VSTR + 4 * (col & 3);
+
+    // this wave's pairs: pages c*CH + 2*(wave + 4*j) + {0, 1}
+    const int pstart = c * ch_pages + kPair * wave;
+    const int pstep = kPair * kWaves;
+    PairRegs pr;
+    if (pstart < p_end) pair_load(pr, kpool, vpool, btrow, pstart, p_end, hkv, kvh, num_pages);
+    for (int p0 = pstart; p0 < p_end; p0 += pstep) {
+        bool ok[kPair];
+#pragma unroll
+        for (int j = 0; j < kPair; ++j) ok[j] = pr.ok[j];
+        // V of this pair -> LDS (as loaded; an absent page as zeros), then
+        // K -> S^T on the matrix core (scores of an absent page are masked)
+#pragma unroll
+        for (int j = 0; j < kPair; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                *reinterpret_cast<uint4 *>(vbuf + (16 * j + 4 * i + grp) * VSTR + 8 * col) = sel4(pr.ok[j], pr.v[j][i]);
+        f32x4 sc[kPair];
+#pragma unroll
+        for (int j = 0; j < kPair; ++j) {
+            sc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+                sc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, pr.k[j][kb]),
+                                                                __builtin_bit_cast(bf16x8, qop[kb]), sc[j], 0, 0, 0);
+        }
+        // next pair's loads go out while this pair is finished
+        const int pn = p0 + pstep;
+        if (pn < p_end) pair_load(pr, kpool, vpool, btrow, pn, p_end, hkv, kvh, num_pages);
+
+        // mask keys past the sequence or on an absent page, then the pair's
+        // maximum per head
+        float mx = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < kPair; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int tok = (p0 + j) * kPageSize + 4 * grp + i;
+                const float v = (ok[j] && tok < L) ? sc[j][i] * scale_log2 : -INFINITY;
+                sc[j][i] = v;
+                mx = fmaxf(mx, v);
+            }
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        if (__builtin_amdgcn_ballot_w64(mx > m_run + kRescaleLog2) != 0) {
+            const float m_new = fmaxf(m_run, mx);
+            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+            m_run = m_new;
+            l_run *= alpha;
+#pragma unroll
+            for (int db = 0; db < 8; ++db) oacc[db] *= alpha;
+        }
+        float p[kPair][4];
+#pragma unroll
+        for (int j = 0; j < kPair; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                p[j][i] = __builtin_amdgcn_exp2f(sc[j][i] - m_run);
+                l_run += p[j][i];
+            }
+        // P^T operand: k-slot e < 4 is token 4grp+e of page 0, e >= 4 token
+        // 16 + 4grp + e-4 of page 1 -- the V^T reads below use the same order
+        const uint4 pop = make_uint4(cvt2(p[0][0], p[0][1]), cvt2(p[0][2], p[0][3]),
+                                     cvt2(p[1][0], p[1][1]), cvt2(p[1][2], p[1][3]));
+#pragma unroll
+        for (int db = 0; db < 8; ++db) {
+            const i16x4 lo = lds_read_tr(vtr + 16 * db);
+            const i16x4 hi = lds_read_tr(vtr + 16 * VSTR + 16 * db);
+            const bf16x8 a = __builtin_bit_cast(
+                bf16x8, make_uint4(__builtin_bit_cast(uint2, lo).x, __builtin_bit_cast(uint2, lo).y,
+                                   __builtin_bit_cast(uint2, hi).x, __builtin_bit_cast(uint2, hi).y));
+            oacc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, pop), oacc[db], 0, 0, 0);
+        }
+    }
+
+    // ---- merge the 4 waves: per-head (m, l) and O^T through LDS
+    l_run += __shfl_xor(l_run, 16);
+    l_run += __shfl_xor(l_run, 32);
+    if (grp == 0) {
+        s_m[wave][col] = m_run;
+        s_l[wave][col] = l_run;
+    }
+    __syncthreads();  // every wave is done with its V buffer: reuse it for O^T
+    float *s_o = reinterpret_cast<float *>(s_v);  // [kWaves][128 d][16 heads]
+#pragma unroll
+    for (int db = 0; db < 8; ++db)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) s_o[(wave * kHeadDim + 16 * db + 4 * grp + i) * 16 + col] = oacc[db][i];
+    __syncthreads();
+    for (int idx = tid; found && idx < group * kHeadDim; idx += kThreads) {
+        const int h = idx / kHeadDim, d = idx % kHeadDim;
+        float M = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w][h]);
+        float lsum = 0.f, o = 0.f;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+            const float mw = s_m[w][h];
+            const float wt = mw == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mw - M);  // waves without pages
+            lsum += wt * s_l[w][h];
+            o += wt * s_o[(w * kHeadDim + d) * 16 + h];
+        }
+        if (nch == 1) {
+            out[(static_cast<size_t>(b) * hq + kvh * group + h) * kHeadDim + d] = to_bf16(o / lsum);
+        } else {
+            ws_o[(static_cast<size_t>(u) * group + h) * kHeadDim + d] = o;
+            if (d == 0) ws_ml[static_cast<size_t>(u) * group + h] = make_float2(M, lsum);
+        }
+    }
+    if (found && c == 0 && kvh == 0 && tid == 0) ws_cbase[b] = first;
+}
+
+}  // namespace dk
+}  // namespace

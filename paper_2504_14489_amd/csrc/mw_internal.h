@@ -70,3 +70,33 @@ void timing_end(mw_timing *t);
 mw_status check_launch(const char *what);
 
 }  // namespace mw
+
+namespace mw {
+
+// Checked launch parameters of one decode call (shared by mw_decode_attn and
+// the fused kernel's launcher).
+struct DecodePlan {
+    int64_t units;        // (chunk, kv head) work units of the split kernel
+    int chunk_pages;      // resolved chunk length (0 chooses from the lengths)
+    size_t off_ml, off_cbase, bytes;  // workspace layout: partial O, (m, l), chunk bases
+    int hkv, group;
+    float scale_log2;
+};
+// Validates a decode call's arguments (workspace size included) and plans it.
+mw_status decode_prepare(const mw_decode_args *a, DecodePlan *p, const char *who);
+// Launches the kernel that merges the chunk partials of every (sequence, kv head).
+mw_status decode_combine_launch(const mw_decode_args *a, const DecodePlan &p, hipStream_t s);
+
+// Checked launch parameters of one prefill call.
+struct PrefillPlan {
+    int hkv, group, n_hgroups, paired;
+    int64_t gx;           // work-groups per sequence (grid x); 0: nothing to do
+    int batch;
+    bool table_in_lds;    // every block-table entry a work-group needs fits its LDS copy
+    float scale_log2;
+};
+// Validates a prefill call's arguments and plans it for a stream that may use
+// `cus` CUs (block pairing depends on it).
+mw_status prefill_prepare(const mw_prefill_args *a, int64_t cus, PrefillPlan *p, const char *who);
+
+}  // namespace mw

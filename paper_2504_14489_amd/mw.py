@@ -151,6 +151,7 @@ _SIGNATURES = {
                        ctypes.POINTER(EnginePlan), ctypes.POINTER(EngineStats)], _I),
     "mw_engine_timeline": ([_P, _I, _PD, _I, _PI], _I),
     "mw_engine_graphs": ([_P, _PI, ctypes.POINTER(ctypes.c_int64), _PD], _I),
+    "mw_fused_attn": ([ctypes.POINTER(_PrefillArgs), ctypes.POINTER(_DecodeArgs), _P, _P], _I),
 }
 
 EXPORTED = tuple(_SIGNATURES)
@@ -480,11 +481,8 @@ def mw_engine_memory(eng) -> Tuple[int, float]:
     return b.value, ms.value
 
 
-def mw_engine_run(eng, dec: dict, pre: dict, plan: EnginePlan) -> dict:
-    """dec: pool, hq, hkv, head_dim, scale, seq_lens (host), d_seq_lens, d_block_table,
-    bt_stride, d_q, d_out, d_workspace, workspace_bytes, chunk_pages;
-    pre: pool, hq, hkv, head_dim, scale, new_lens, prefix_lens (host), d_qo_indptr,
-    d_prefix_lens, d_block_table, bt_stride, d_q, d_out.  Returns the stats as a dict."""
+def _engine_structs(dec: dict, pre: dict):
+    """ctypes argument structs (and the host arrays they point at) from dicts."""
     sl = _i32(dec["seq_lens"])
     nl, pl = _i32(pre["new_lens"]), _i32(pre["prefix_lens"])
     da = _DecodeArgs(_h(dec["pool"]), _shape(dec["hq"], dec["hkv"], dec["head_dim"], dec["scale"]), len(sl),
@@ -494,6 +492,21 @@ def mw_engine_run(eng, dec: dict, pre: dict, plan: EnginePlan) -> dict:
     pa = _PrefillArgs(_h(pre["pool"]), _shape(pre["hq"], pre["hkv"], pre["head_dim"], pre["scale"]), len(nl),
                       nl.ctypes.data, pl.ctypes.data, _h(pre["d_qo_indptr"]), _h(pre["d_prefix_lens"]),
                       _h(pre["d_block_table"]), pre["bt_stride"], _h(pre["d_q"]), _h(pre["d_out"]))
+    return da, pa, (sl, nl, pl)
+
+
+def mw_fused_attn(pre: dict, dec: dict, stream=0, timing=None):
+    """One fused prefill + decode launch; dicts as for :func:`mw_engine_run`."""
+    da, pa, keep = _engine_structs(dec, pre)
+    _check(load().mw_fused_attn(ctypes.byref(pa), ctypes.byref(da), _h(stream), _h(timing)))
+
+
+def mw_engine_run(eng, dec: dict, pre: dict, plan: EnginePlan) -> dict:
+    """dec: pool, hq, hkv, head_dim, scale, seq_lens (host), d_seq_lens, d_block_table,
+    bt_stride, d_q, d_out, d_workspace, workspace_bytes, chunk_pages;
+    pre: pool, hq, hkv, head_dim, scale, new_lens, prefix_lens (host), d_qo_indptr,
+    d_prefix_lens, d_block_table, bt_stride, d_q, d_out.  Returns the stats as a dict."""
+    da, pa, keep = _engine_structs(dec, pre)
     st = EngineStats()
     _check(load().mw_engine_run(eng, ctypes.byref(da), ctypes.byref(pa), ctypes.byref(plan), ctypes.byref(st)))
     return st.as_dict()
