@@ -237,13 +237,17 @@ class Bench:
         self.dw.close()
 
 
-KERNEL_SOURCES = {"k_prefill_attn": "prefill_attn.hip", "k_decode_split": "decode_attn.hip"}
+KERNEL_SOURCES = {"k_prefill_attn": ("prefill_attn.hip", "prefill_block.h"),
+                  "k_decode_split": ("decode_attn.hip", "decode_block.h")}
 
 
 def source_sha(kernel):
+    """Hash of the kernel's sources (launcher and work-group body)."""
     import hashlib
-    path = os.path.join(ROOT, "paper_2504_14489_amd", "csrc", KERNEL_SOURCES[kernel])
-    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES[kernel]:
+        h.update(open(os.path.join(ROOT, "paper_2504_14489_amd", "csrc", name), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def committed_traffic(kernel, workload):

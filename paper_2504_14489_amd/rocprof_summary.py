@@ -1,0 +1,151 @@
+"""Short text summaries of rocprofv3 output for the committed profiles.
+
+    python -m paper_2504_14489_amd.rocprof_summary traffic --workload llama8b \\
+        --fetch <dir of the FETCH_SIZE run> --write <dir of the WRITE_SIZE run> --out profiles/traffic_llama8b.txt
+    python -m paper_2504_14489_amd.rocprof_summary trace --stats-dir <dir of a --kernel-trace --stats run> \\
+        --title "..." --command "..." --out profiles/kernel_trace_llama8b.md
+
+The traffic summary scales each kernel's FETCH_SIZE / WRITE_SIZE (KiB per
+dispatch) by what the same counter reads for the runtime's device copy of a
+known size in the same run, and records the kernel sources' hash so that a
+reader (bench.py) can tell when the figures no longer describe the kernel.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import os
+import re
+import statistics
+import sys
+from collections import defaultdict
+
+COPY_KERNEL = "__amd_rocclr_copyBuffer"
+COPY_BYTES = 256 << 20        # the copy bench.py --traffic-pass makes
+
+
+def _rows(d: str, suffix: str):
+    files = sorted(glob.glob(os.path.join(d, "**", f"*{suffix}"), recursive=True))
+    if not files:
+        raise SystemExit(f"no *{suffix} under {d}")
+    for f in files:
+        with open(f, newline="") as fh:
+            yield from csv.DictReader(fh)
+
+
+def _short(name: str) -> str:
+    """Kernel name without template arguments, parameters or namespaces."""
+    name = re.sub(r"\(.*$", "", name)
+    name = re.sub(r"<.*>", "", name)
+    return name.split("::")[-1].strip()
+
+
+def counter_per_dispatch(d: str, counter: str):
+    """kernel -> list of the counter's value per dispatch (summed over the
+    rows a dispatch has, e.g. one per XCD)."""
+    per = defaultdict(float)
+    names = {}
+    for r in _rows(d, "counter_collection.csv"):
+        if r.get("Counter_Name") != counter:
+            continue
+        key = r.get("Dispatch_Id") or r.get("Correlation_Id")
+        per[key] += float(r["Counter_Value"])
+        names[key] = _short(r["Kernel_Name"])
+    out = defaultdict(list)
+    for k, v in per.items():
+        out[names[k]].append(v)
+    return out
+
+
+def traffic(args):
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    from bench import source_sha, KERNEL_SOURCES
+    fetch = counter_per_dispatch(args.fetch, "FETCH_SIZE")
+    write = counter_per_dispatch(args.write, "WRITE_SIZE")
+    if COPY_KERNEL not in fetch or COPY_KERNEL not in write:
+        raise SystemExit("the calibration copy is missing from the counter runs")
+    kib = COPY_BYTES / 1024
+    f_scale = kib / statistics.median(fetch[COPY_KERNEL])
+    w_scale = kib / statistics.median(write[COPY_KERNEL])
+    lines = [f"# HBM traffic per launch: {args.workload} workload", "",
+             "Commands (on the MI355X box, from /tmp with TMPDIR=/tmp; one counter per run):", "",
+             f"    rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_FETCH_SIZE -o run -- "
+             f"python3 bench.py --config {args.workload} --traffic-pass",
+             f"    rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_WRITE_SIZE -o run -- "
+             f"python3 bench.py --config {args.workload} --traffic-pass",
+             f"    python -m paper_2504_14489_amd.rocprof_summary traffic --workload {args.workload} "
+             f"--fetch gpurun_out/pmc_FETCH_SIZE --write gpurun_out/pmc_WRITE_SIZE --out <this file>", "",
+             "bench.py --traffic-pass runs one isolated launch of each kernel on its partition and a "
+             f"device-to-device copy of {COPY_BYTES} bytes ({COPY_KERNEL}) that calibrates the counters.", "",
+             f"# copy calibration: FETCH_SIZE read {statistics.median(fetch[COPY_KERNEL]):.1f} KiB and WRITE_SIZE "
+             f"{statistics.median(write[COPY_KERNEL]):.1f} KiB for {kib:.0f} KiB moved",
+             f"copy.fetch_scale: {f_scale:.4f}", f"copy.write_scale: {w_scale:.4f}", ""]
+    for k in sorted(set(fetch) & set(write)):
+        if k == COPY_KERNEL or not k.startswith("k_"):
+            continue
+        fk, wk = statistics.median(fetch[k]), statistics.median(write[k])
+        tb = (fk * f_scale + wk * w_scale) * 1024
+        lines += [f"# {k}: FETCH_SIZE {fk:.1f} KiB, WRITE_SIZE {wk:.1f} KiB per dispatch (raw, median of "
+                  f"{len(fetch[k])})", f"{k}.fetch_kib: {fk:.3f}", f"{k}.write_kib: {wk:.3f}",
+                  f"{k}.traffic_bytes: {tb:.0f}"]
+        if k in KERNEL_SOURCES:
+            lines.append(f"{k}.source_sha256_16: {source_sha(k)}")
+        lines.append("")
+    with open(args.out, "w") as f:
+        f.write("\n".join(lines))
+    print("\n".join(lines))
+
+
+def trace(args):
+    rows = list(_rows(args.stats_dir, "kernel_stats.csv"))
+    tot = sum(float(r["TotalDurationNs"]) for r in rows)
+    lines = [f"# {args.title}", "", "Command (on the MI355X box, from /tmp with TMPDIR=/tmp):", "",
+             f"    {args.command}", "", "## --stats summary (all dispatches of the run)", "",
+             "| kernel | calls | average (us) | min (us) | max (us) | share of GPU time |",
+             "|---|---|---|---|---|---|"]
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        lines.append(f"| {_short(r['Name'])[:40]} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                     f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | "
+                     f"{100 * float(r['TotalDurationNs']) / tot:.1f}% |")
+    if args.trace_last:
+        # per-dispatch durations of the last N dispatches of each kernel
+        disp = defaultdict(list)
+        for r in _rows(args.stats_dir, "kernel_trace.csv"):
+            disp[_short(r["Kernel_Name"])].append(
+                (int(r["Start_Timestamp"]), int(r["End_Timestamp"]) - int(r["Start_Timestamp"])))
+        lines += ["", f"## The last {args.trace_last} dispatches of each kernel (the timed region)", "",
+                  "| kernel | mean (us) | median (us) |", "|---|---|---|"]
+        for k in args.kernels.split(","):
+            if k in disp:
+                last = [d for _, d in sorted(disp[k])[-args.trace_last:]]
+                lines.append(f"| {k} | {statistics.mean(last) / 1e3:.1f} | {statistics.median(last) / 1e3:.1f} |")
+    if args.note:
+        lines += ["", args.note]
+    with open(args.out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    t = sub.add_parser("traffic")
+    t.add_argument("--workload", required=True)
+    t.add_argument("--fetch", required=True)
+    t.add_argument("--write", required=True)
+    t.add_argument("--out", required=True)
+    k = sub.add_parser("trace")
+    k.add_argument("--stats-dir", required=True)
+    k.add_argument("--title", required=True)
+    k.add_argument("--command", required=True)
+    k.add_argument("--trace-last", type=int, default=0)
+    k.add_argument("--kernels", default="k_prefill_attn,k_decode_split")
+    k.add_argument("--note", default="")
+    k.add_argument("--out", required=True)
+    args = ap.parse_args(argv)
+    traffic(args) if args.cmd == "traffic" else trace(args)
+
+
+if __name__ == "__main__":
+    main()
