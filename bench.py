@@ -483,7 +483,10 @@ def main():
     base = {k: v[0] for k, v in res.items()}
     spatial = results[0]["ms_per_step"]
     spatial_dec = results[0]["mux"]["decode_call_ms"]
+    best = min((r for r in results if r["decode_iters_per_step"] == m), key=lambda r: r["ms_per_step"])
     baselines = {"spatial_ms_per_step": spatial, "serial_ms_per_step": base["serial"],
+                 "spatial_best_ms_per_step": best["ms_per_step"],
+                 "spatial_best_split": [best["prefill_cus"], best["decode_cus"]],
                  "free_streams_ms_per_step": base["free"], "fused_ms_per_step": base["fused"],
                  "spatial_speedup": {k: base[k] / spatial for k in base},
                  "decode_iteration_ms": {"spatial": spatial_dec, **{k: v[1] for k, v in res.items()}}}

@@ -36,6 +36,8 @@ def _rows(d: str, suffix: str):
 
 def _short(name: str) -> str:
     """Kernel name without template arguments, parameters or namespaces."""
+    name = name.replace("(anonymous namespace)::", "")
+    name = re.sub(r"^void ", "", name.strip())
     name = re.sub(r"\(.*$", "", name)
     name = re.sub(r"<.*>", "", name)
     return name.split("::")[-1].strip()
@@ -66,8 +68,10 @@ def traffic(args):
     if COPY_KERNEL not in fetch or COPY_KERNEL not in write:
         raise SystemExit("the calibration copy is missing from the counter runs")
     kib = COPY_BYTES / 1024
-    f_scale = kib / statistics.median(fetch[COPY_KERNEL])
-    w_scale = kib / statistics.median(write[COPY_KERNEL])
+    # the calibration copy is the largest copy of the run (the others upload
+    # the workload's small arrays)
+    f_copy, w_copy = max(fetch[COPY_KERNEL]), max(write[COPY_KERNEL])
+    f_scale, w_scale = kib / f_copy, kib / w_copy
     lines = [f"# HBM traffic per launch: {args.workload} workload", "",
              "Commands (on the MI355X box, from /tmp with TMPDIR=/tmp; one counter per run):", "",
              f"    rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_FETCH_SIZE -o run -- "
@@ -78,8 +82,8 @@ def traffic(args):
              f"--fetch gpurun_out/pmc_FETCH_SIZE --write gpurun_out/pmc_WRITE_SIZE --out <this file>", "",
              "bench.py --traffic-pass runs one isolated launch of each kernel on its partition and a "
              f"device-to-device copy of {COPY_BYTES} bytes ({COPY_KERNEL}) that calibrates the counters.", "",
-             f"# copy calibration: FETCH_SIZE read {statistics.median(fetch[COPY_KERNEL]):.1f} KiB and WRITE_SIZE "
-             f"{statistics.median(write[COPY_KERNEL]):.1f} KiB for {kib:.0f} KiB moved",
+             f"# copy calibration: FETCH_SIZE read {f_copy:.1f} KiB and WRITE_SIZE {w_copy:.1f} KiB for "
+             f"{kib:.0f} KiB moved",
              f"copy.fetch_scale: {f_scale:.4f}", f"copy.write_scale: {w_scale:.4f}", ""]
     for k in sorted(set(fetch) & set(write)):
         if k == COPY_KERNEL or not k.startswith("k_"):
@@ -114,11 +118,14 @@ def trace(args):
         for r in _rows(args.stats_dir, "kernel_trace.csv"):
             disp[_short(r["Kernel_Name"])].append(
                 (int(r["Start_Timestamp"]), int(r["End_Timestamp"]) - int(r["Start_Timestamp"])))
-        lines += ["", f"## The last {args.trace_last} dispatches of each kernel (the timed region)", "",
+        skip = f" before the last {args.skip_last}" if args.skip_last else ""
+        lines += ["", f"## The last {args.trace_last} dispatches{skip} of each kernel (the timed region)", "",
                   "| kernel | mean (us) | median (us) |", "|---|---|---|"]
         for k in args.kernels.split(","):
             if k in disp:
-                last = [d for _, d in sorted(disp[k])[-args.trace_last:]]
+                seq = [d for _, d in sorted(disp[k])]
+                seq = seq[:len(seq) - args.skip_last] if args.skip_last else seq
+                last = seq[-args.trace_last:]
                 lines.append(f"| {k} | {statistics.mean(last) / 1e3:.1f} | {statistics.median(last) / 1e3:.1f} |")
     if args.note:
         lines += ["", args.note]
@@ -140,6 +147,7 @@ def main(argv=None):
     k.add_argument("--title", required=True)
     k.add_argument("--command", required=True)
     k.add_argument("--trace-last", type=int, default=0)
+    k.add_argument("--skip-last", type=int, default=0)
     k.add_argument("--kernels", default="k_prefill_attn,k_decode_split")
     k.add_argument("--note", default="")
     k.add_argument("--out", required=True)
