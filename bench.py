@@ -507,6 +507,8 @@ def main():
                    "2048-token prefill chunk (no prefix) + 64 decodes with contexts U[512,4096]",
         "llama70b": "Llama-3-70B-shaped attention layer: 64 q-heads/8 kv-heads; 8192-token prefill in "
                     "four 2048-token chunks + 128 decodes, lognormal contexts (median 2048, sigma 0.8)",
+        "llama70b_tp8": "one GPU's tensor-parallel-8 shard of the Llama-3-70B attention layer: 8 q-heads/1 kv-head; "
+                        "8192-token prefill in four 2048-token chunks + 128 decodes, lognormal contexts",
         "longctx8b": "8B shapes, long context: 4096 new tokens over a 28672-token prefix + 32 decodes "
                      "U[16384,32768]",
         "sweep8b": "8B shapes: 4096-token prefill + 256 decodes U[1024,8192], prefill CU sweep",

@@ -4,6 +4,8 @@
         --fetch <dir of the FETCH_SIZE run> --write <dir of the WRITE_SIZE run> --out profiles/traffic_llama8b.txt
     python -m paper_2504_14489_amd.rocprof_summary trace --stats-dir <dir of a --kernel-trace --stats run> \\
         --title "..." --command "..." --out profiles/kernel_trace_llama8b.md
+    python -m paper_2504_14489_amd.rocprof_summary mfma --dir <dir of the MFMA counter run> --workload llama8b \\
+        --cus 64 --out profiles/mfma_llama8b.txt
 
 The traffic summary scales each kernel's FETCH_SIZE / WRITE_SIZE (KiB per
 dispatch) by what the same counter reads for the runtime's device copy of a
@@ -23,6 +25,7 @@ from collections import defaultdict
 
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 COPY_BYTES = 256 << 20        # the copy bench.py --traffic-pass makes
+N_XCD = 8                     # accelerator dies of an MI355X
 
 
 def _rows(d: str, suffix: str):
@@ -101,6 +104,45 @@ def traffic(args):
     print("\n".join(lines))
 
 
+def mfma(args):
+    """Matrix-core use of k_prefill_attn from SQ_INSTS_VALU_MFMA_MOPS_BF16 (512 flop
+    each), SQ_VALU_MFMA_BUSY_CYCLES (summed over SIMDs) and GRBM_GUI_ACTIVE."""
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    from bench import source_sha
+    from paper_2504_14489_amd import accounting, workloads as W
+    cfg = W.CONFIGS[args.workload]
+    vals = {c: counter_per_dispatch(args.dir, c) for c in
+            ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE")}
+    k = "k_prefill_attn"
+    mops = statistics.median(vals["SQ_INSTS_VALU_MFMA_MOPS_BF16"][k])
+    busy = statistics.median(vals["SQ_VALU_MFMA_BUSY_CYCLES"][k])
+    # the CSV sums GRBM_GUI_ACTIVE over the 8 XCDs; each XCD counts the same
+    # dispatch, so one XCD's count is the dispatch's duration in cycles
+    active = statistics.median(vals["GRBM_GUI_ACTIVE"][k]) / N_XCD
+    algo = accounting.prefill_flops(cfg.hq, cfg.head_dim, [cfg.pre_chunks[0]])
+    simds = 4 * args.cus
+    lines = [f"# Matrix-core use of k_prefill_attn: {args.workload} workload, first prefill chunk on {args.cus} CUs",
+             "", "Commands (on the MI355X box, from /tmp with TMPDIR=/tmp):", "",
+             f"    rocprofv3 --pmc SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE "
+             f"--output-format csv -d gpurun_out/pmc_mfma -o run -- python3 bench.py --config {args.workload} "
+             f"--traffic-pass",
+             f"    python -m paper_2504_14489_amd.rocprof_summary mfma --dir gpurun_out/pmc_mfma --workload "
+             f"{args.workload} --cus {args.cus} --out <this file>", "",
+             f"k_prefill_attn.mfma_bf16_flop: {mops * 512:.0f}",
+             f"k_prefill_attn.algorithmic_flop: {algo:.0f}",
+             f"k_prefill_attn.executed_over_algorithmic: {mops * 512 / algo:.4f}",
+             f"k_prefill_attn.mfma_busy_cycles_sum: {busy:.0f}",
+             f"k_prefill_attn.gui_active_cycles_per_xcd: {active:.0f}",
+             f"k_prefill_attn.mfma_busy_fraction_of_partition_simds: {busy / (active * simds):.4f}",
+             f"k_prefill_attn.source_sha256_16: {source_sha(k)}", "",
+             "executed / algorithmic > 1: the MFMAs of masked key tiles on the diagonal and of padding rows.",
+             "busy fraction: SQ_VALU_MFMA_BUSY_CYCLES over GRBM_GUI_ACTIVE times the partition's SIMDs "
+             f"({simds}).", ""]
+    with open(args.out, "w") as f:
+        f.write("\n".join(lines))
+    print("\n".join(lines))
+
+
 def trace(args):
     rows = list(_rows(args.stats_dir, "kernel_stats.csv"))
     tot = sum(float(r["TotalDurationNs"]) for r in rows)
@@ -151,8 +193,13 @@ def main(argv=None):
     k.add_argument("--kernels", default="k_prefill_attn,k_decode_split")
     k.add_argument("--note", default="")
     k.add_argument("--out", required=True)
+    m = sub.add_parser("mfma")
+    m.add_argument("--dir", required=True)
+    m.add_argument("--workload", required=True)
+    m.add_argument("--cus", type=int, required=True)
+    m.add_argument("--out", required=True)
     args = ap.parse_args(argv)
-    traffic(args) if args.cmd == "traffic" else trace(args)
+    {"traffic": traffic, "trace": trace, "mfma": mfma}[args.cmd](args)
 
 
 if __name__ == "__main__":

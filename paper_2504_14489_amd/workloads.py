@@ -118,6 +118,11 @@ CONFIGS = {
     "llama70b": Config("llama70b", 64, 8,
                        ((0, 2048), (2048, 2048), (4096, 2048), (6144, 2048)),
                        128, "lognormal", 64, 16384, None, (96,), (160,)),
+    # one GPU's shard of the Llama-3-70B layer at tensor-parallel degree 8
+    # (8 q-heads / 1 kv-head per GPU), same tokens and decode batch as llama70b
+    "llama70b_tp8": Config("llama70b_tp8", 8, 1,
+                           ((0, 2048), (2048, 2048), (4096, 2048), (6144, 2048)),
+                           128, "lognormal", 64, 16384, None, (96,), (160,)),
     # long context 8B: 4096 new tokens over a 28672-token cached prefix;
     # 32 decodes in [16384, 32768]
     "longctx8b": Config("longctx8b", 32, 8, ((28672, 4096),), 32, "uniform",

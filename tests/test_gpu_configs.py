@@ -27,7 +27,7 @@ def sample_seqs(lens, k=6):
     return sorted(idx)
 
 
-@pytest.mark.parametrize("name", ["llama8b", "llama70b", "longctx8b", "sweep8b"])
+@pytest.mark.parametrize("name", ["llama8b", "llama70b", "llama70b_tp8", "longctx8b", "sweep8b"])
 def test_full_size_config(name):
     cfg = W.CONFIGS[name]
     say(f"full-size {name}: generating")

@@ -24,7 +24,7 @@ def test_bf16_rounding_matches_torch():
         torch.bfloat16).float().numpy())
 
 
-@pytest.mark.parametrize("name", ["tiny", "llama8b", "llama70b", "longctx8b", "sweep8b"])
+@pytest.mark.parametrize("name", ["tiny", "llama8b", "llama70b", "llama70b_tp8", "longctx8b", "sweep8b"])
 def test_decode_lengths_follow_the_config(name):
     cfg = W.CONFIGS[name]
     L = W.draw_decode_lengths(cfg, np.random.Generator(np.random.PCG64(0)))
