@@ -117,14 +117,20 @@ def write_table(out: Dict, path: str, argv):
     cmd = "python -m paper_2504_14489_amd.engine " + " ".join(argv)
     g, dg = out["group"], out.get("decode_graphs", {})
     lines = [f"# Multiplex engine, workload {out['workload']} (N_T = {out['model_layers']} calls per decode iteration)",
-             "", f"Command: `{cmd}`", "",
+             "", f"Command: `{cmd}`", "", f"N_PL from: {out['n_pl_from']}.", "",
              f"Partition group: {g['partitions']} partition(s) + whole-device stream, "
              f"{g['device_bytes'] / 2**20:.2f} MiB device memory, created in {g['create_ms']:.2f} ms.",
              f"Decode graphs: {dg.get('graphs', 0)}, {dg.get('device_bytes', 0) / 2**20:.2f} MiB, "
              f"{dg.get('capture_ms', 0.0):.2f} ms to capture, instantiate and upload.", ""]
     for p in out["partitions"]:
         lines += [f"## Prefill on {p['prefill_cus']} CUs (solo: decode call {p['decode_layer_ms']:.3f} ms, "
-                  f"prefill call {p['prefill_layer_ms']:.3f} ms)", "",
+                  f"prefill call {p['prefill_layer_ms']:.3f} ms)", ""]
+        if "estimate" in p:
+            e = p["estimate"]
+            lines += [f"Estimator (N_PL from it): prefill call {e['prefill_layer_ms_solo']:.3f} ms, decode call "
+                      f"{e['decode_layer_ms_solo']:.3f} ms solo x guard {e['guard_slowdown']:.3f} = "
+                      f"{e['decode_layer_ms_worst']:.3f} ms worst case.", ""]
+        lines += [
                   f"Layer-wise launch overhead on the prefill end, steady scenario: N_PL from the formula "
                   f"{100 * p['layerwise_overhead_npl']:+.2f}%, one layer per launch "
                   f"{100 * p['layerwise_overhead']:+.2f}% (both against the whole job in one launch).", "",
@@ -147,6 +153,44 @@ def write_table(out: Dict, path: str, argv):
         f.write("\n".join(lines))
 
 
+class Estimate:
+    """The contention-tolerant estimator (paper Sec. 3.3) built from a profiling
+    run (paper_2504_14489_amd.profiling --out): solo-run predictor fitted on the
+    grid samples, contention guard over the measured pairs; worst case =
+    solo prediction x guard slowdown."""
+
+    def __init__(self, path: str):
+        with open(path) as f:
+            prof = json.load(f)
+        self.model = prof["model"]
+        self.p = mw.mw_predictor_create()
+        self.g = mw.mw_guard_create()
+        for smp in prof["prefill"]:
+            if smp["grid"]:
+                mw.mw_predictor_add_prefill(self.p, smp["cus"], [smp["n"]], [smp["r"]], smp["ms"])
+        for smp in prof["decode"]:
+            if smp["grid"]:
+                mw.mw_predictor_add_decode(self.p, smp["cus"], smp["lens"], smp["ms"])
+        mw.mw_predictor_fit(self.p)
+        for smp in prof["pairs"]:
+            if smp["slowdown"] is not None:
+                mw.mw_guard_add(self.g, smp["prefill_new"], smp["prefill_reused"], smp["decode_batch"],
+                                smp["decode_reused"], smp["prefill_cus"], smp["slowdown"])
+
+    def layers(self, prefill_cus: int, new_lens, prefix_lens, dec_lens):
+        """(solo prefill ms, solo decode ms, guard slowdown) of one prefill and
+        one decode attention call on a prefill_cus / 256 - prefill_cus split."""
+        t_p = mw.mw_predictor_prefill_ms(self.p, prefill_cus, new_lens, prefix_lens)
+        t_d = mw.mw_predictor_decode_ms(self.p, 256 - prefill_cus, dec_lens)
+        slow = mw.mw_guard_lookup(self.g, int(sum(new_lens)), int(sum(prefix_lens)), len(dec_lens),
+                                  int(sum(int(L) - 1 for L in dec_lens)), prefill_cus)
+        return t_p, t_d, slow
+
+    def close(self):
+        mw.mw_predictor_destroy(self.p)
+        mw.mw_guard_destroy(self.g)
+
+
 def main(argv=None):
     import torch
     from . import workloads as W
@@ -162,6 +206,9 @@ def main(argv=None):
     ap.add_argument("--reps", type=int, default=3)
     ap.add_argument("--out", default="")
     ap.add_argument("--table", default="", help="also write a Markdown summary here")
+    ap.add_argument("--profile", default="",
+                    help="a profiling run's JSON: N_PL then comes from the estimator's worst-case latencies "
+                         "instead of this run's solo measurements")
     argv = sys.argv[1:] if argv is None else list(argv)
     args = ap.parse_args(argv)
 
@@ -172,6 +219,15 @@ def main(argv=None):
     dec, pre = dw.engine_args()
     L = args.model_layers
     out: Dict = {"workload": cfg.name, "model_layers": L, "partitions": []}
+    est = None
+    if args.profile:
+        est = Estimate(args.profile)
+        m = est.model
+        if (m["num_q_heads"], m["num_kv_heads"], m["head_dim"]) != (cfg.hq, cfg.hkv, cfg.head_dim):
+            raise SystemExit("the profile was taken for another model shape")
+        out["n_pl_from"] = "estimator (solo-run prediction x contention guard)"
+    else:
+        out["n_pl_from"] = "solo latencies measured on the partition"
 
     torch.cuda.synchronize()
     free0 = torch.cuda.mem_get_info()[0]
@@ -211,10 +267,18 @@ def main(argv=None):
             t_d, t_p = td.elapsed()[0], tp.elapsed()[0]
             log(f"[engine] partition {p_cus}: decode layer {t_d:.3f} ms, prefill layer {t_p:.3f} ms")
             part = {"prefill_cus": p_cus, "decode_layer_ms": t_d, "prefill_layer_ms": t_p, "scenarios": {}}
+            e_d, e_p = t_d, t_p
+            if est is not None:
+                sp, sd, slow = est.layers(p_cus, pre["new_lens"], pre["prefix_lens"], dw.dec_lens)
+                # worst case: decode slowed by the guard; prefill at its solo prediction
+                e_d, e_p = sd * slow, sp
+                part["estimate"] = {"prefill_layer_ms_solo": sp, "decode_layer_ms_solo": sd, "guard_slowdown": slow,
+                                    "decode_layer_ms_worst": e_d}
+                log(f"[engine] estimator: prefill layer {sp:.3f} ms, decode layer {sd:.3f} ms x guard {slow:.3f}")
             for sc_name, (d_layers, d_iters, p_layers, variants) in scenarios(L, args).items():
-                # N_PL = ceil(T_d * N_T / T_P) with the solo latencies of one
-                # decode iteration and of one N_T-layer prefill job
-                n_pl = mw.mw_prefill_layers(t_d * d_layers, t_p * L, L)
+                # N_PL = ceil(T_d * N_T / T_P) with the latencies of one decode
+                # iteration and of one N_T-layer prefill job
+                n_pl = mw.mw_prefill_layers(e_d * d_layers, e_p * L, L)
                 sc = {"decode_layers": d_layers, "decode_iters": d_iters, "prefill_layers": p_layers,
                       "n_pl": n_pl, "runs": {}}
                 for name in variants:
@@ -249,6 +313,8 @@ def main(argv=None):
     finally:
         eng.close()
         dw.close()
+        if est is not None:
+            est.close()
     line = json.dumps(out)
     print(line, flush=True)
     if args.out:

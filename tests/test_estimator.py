@@ -169,3 +169,41 @@ def test_prefill_layers_matches_oracle():
     for bad in ((0.0, 1.0, 32), (1.0, 0.0, 32), (1.0, 1.0, 0), (math.inf, 1.0, 32)):
         with pytest.raises(mw.MWError):
             mw.mw_prefill_layers(*bad)
+
+
+def test_engine_estimate_from_a_profile(tmp_path):
+    """The engine's estimator reads a profiling run: the solo predictions
+    reproduce times generated from Eqs. (1)-(2), and the guard returns the
+    measured slowdown of the matching cell."""
+    import json
+    from paper_2504_14489_amd.engine import Estimate
+    th_p = (2e-8, 1e-8, 3e-5, 0.01)   # ms per n^2, n*r, n, constant
+    th_d = (1e-5, 2e-4, 0.02)         # ms per reused token, per sequence, constant
+
+    def t_pre(n, r):
+        return th_p[0] * n * n + th_p[1] * n * r + th_p[2] * n + th_p[3]
+
+    def t_dec(lens):
+        return th_d[0] * sum(L - 1 for L in lens) + th_d[1] * len(lens) + th_d[2]
+
+    prof = {"model": {"num_q_heads": 32, "num_kv_heads": 8, "head_dim": 128, "page_size": 16},
+            "prefill": [], "decode": [], "pairs": []}
+    for n in (1024, 4096, 16384):
+        for r in (0, 4096, 16384):
+            prof["prefill"].append({"cus": 64, "n": n, "r": r, "ms": t_pre(n, r), "grid": True})
+    for bs in (8, 32, 128):
+        for L in (1024, 4096, 16384):
+            prof["decode"].append({"cus": 192, "lens": [L] * bs, "ms": t_dec([L] * bs), "grid": True})
+    prof["pairs"].append({"prefill_cus": 64, "prefill_new": 2048, "prefill_reused": 0, "decode_batch": 64,
+                          "decode_reused": 64 * 2047, "slowdown": 1.17})
+    path = tmp_path / "profile.json"
+    path.write_text(json.dumps(prof))
+    est = Estimate(str(path))
+    try:
+        lens = [2048] * 64
+        sp, sd, slow = est.layers(64, [2048], [0], lens)
+        assert sp == pytest.approx(t_pre(2048, 0), rel=1e-6)
+        assert sd == pytest.approx(t_dec(lens), rel=1e-6)
+        assert slow == pytest.approx(1.17)
+    finally:
+        est.close()
