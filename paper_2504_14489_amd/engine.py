@@ -130,10 +130,11 @@ def write_table(out: Dict, path: str, argv):
             lines += [f"Estimator (N_PL from it): prefill call {e['prefill_layer_ms_solo']:.3f} ms, decode call "
                       f"{e['decode_layer_ms_solo']:.3f} ms solo x guard {e['guard_slowdown']:.3f} = "
                       f"{e['decode_layer_ms_worst']:.3f} ms worst case.", ""]
+        if "layerwise_overhead" in p:
+            lines += [f"Layer-wise launch overhead on the prefill end, steady scenario: N_PL from the formula "
+                      f"{100 * p['layerwise_overhead_npl']:+.2f}%, one layer per launch "
+                      f"{100 * p['layerwise_overhead']:+.2f}% (both against the whole job in one launch).", ""]
         lines += [
-                  f"Layer-wise launch overhead on the prefill end, steady scenario: N_PL from the formula "
-                  f"{100 * p['layerwise_overhead_npl']:+.2f}%, one layer per launch "
-                  f"{100 * p['layerwise_overhead']:+.2f}% (both against the whole job in one launch).", "",
                   "| scenario | variant | N_PL | wall ms | bubble % (decode / prefill) | decode iteration ms | "
                   "iteration gap us (median / max) | decode launch us | prefill end ms | switched layers | "
                   "switch: GPU gap / host us |", "|---|---|---|---|---|---|---|---|---|---|---|"]
@@ -206,6 +207,8 @@ def main(argv=None):
     ap.add_argument("--reps", type=int, default=3)
     ap.add_argument("--out", default="")
     ap.add_argument("--table", default="", help="also write a Markdown summary here")
+    ap.add_argument("--scenarios", default="", help="comma list: run only these scenarios")
+    ap.add_argument("--variants", default="", help="comma list: run only these variants")
     ap.add_argument("--profile", default="",
                     help="a profiling run's JSON: N_PL then comes from the estimator's worst-case latencies "
                          "instead of this run's solo measurements")
@@ -276,6 +279,10 @@ def main(argv=None):
                                     "decode_layer_ms_worst": e_d}
                 log(f"[engine] estimator: prefill layer {sp:.3f} ms, decode layer {sd:.3f} ms x guard {slow:.3f}")
             for sc_name, (d_layers, d_iters, p_layers, variants) in scenarios(L, args).items():
+                if args.scenarios and sc_name not in args.scenarios.split(","):
+                    continue
+                if args.variants:
+                    variants = [v for v in variants if v in args.variants.split(",")]
                 # N_PL = ceil(T_d * N_T / T_P) with the latencies of one decode
                 # iteration and of one N_T-layer prefill job
                 n_pl = mw.mw_prefill_layers(e_d * d_layers, e_p * L, L)
@@ -303,9 +310,10 @@ def main(argv=None):
                     if not same:
                         raise SystemExit("engine outputs differ from the reference call")
                 part["scenarios"][sc_name] = sc
-            r = part["scenarios"]["steady"]["runs"]
-            part["layerwise_overhead"] = r["polled_layer1"]["prefill_end_ms"] / r["polled_all"]["prefill_end_ms"] - 1
-            part["layerwise_overhead_npl"] = r["polled"]["prefill_end_ms"] / r["polled_all"]["prefill_end_ms"] - 1
+            r = part["scenarios"].get("steady", {}).get("runs", {})
+            if all(k in r for k in ("polled_layer1", "polled_all", "polled")):
+                part["layerwise_overhead"] = r["polled_layer1"]["prefill_end_ms"] / r["polled_all"]["prefill_end_ms"] - 1
+                part["layerwise_overhead_npl"] = r["polled"]["prefill_end_ms"] / r["polled_all"]["prefill_end_ms"] - 1
             out["partitions"].append(part)
         n_g, g_bytes, g_ms = eng.graphs()
         out["decode_graphs"] = {"graphs": n_g, "device_bytes": g_bytes, "capture_ms": g_ms}
