@@ -177,3 +177,33 @@ def test_prefill_wide_score_range():
     got = run_prefill(wl, 0, 200)
     ref = oracle.prefill(wl.q_pre[:200], wl.k_pool, wl.v_pool, wl.pre_bt, 0)
     assert_close(got, ref, "prefill wide score range")
+
+
+def test_empty_batches_and_zero_length_sequences():
+    """Degenerate inputs: no sequences at all, and a zero-length sequence next
+    to a real one in one varlen call (its rows are absent, the other's are
+    exact); nothing is launched for an empty call."""
+    say("prefill/decode empty and zero-length inputs")
+    from paper_2504_14489_amd import mw
+    cfg = W.custom_config(hq=8, hkv=2, pre_chunks=((0, 40),), dec_batch=1, dec_len_lo=1, dec_len_hi=2, seed=77)
+    wl = W.make_workload(cfg)
+    dw = DeviceWorkload(wl)
+    try:
+        dev = dw.device
+        t32 = lambda a: torch.from_numpy(np.asarray(a, dtype=np.int32)).to(dev)
+        # batch 0: both phases return without launching
+        mw.mw_prefill_attn(dw.pool, 8, 2, 128, dw.scale, [], [], 0, 0, 0, 1, 0, 0)
+        nbytes = mw.mw_decode_workspace_size(8, 2, 128, [], 0)
+        ws = torch.zeros(max(nbytes, 16), dtype=torch.uint8, device=dev)
+        mw.mw_decode_attn(dw.pool, 8, 2, 128, dw.scale, [], 0, 0, 1, 0, 0, ws.data_ptr(), ws.numel())
+        # a zero-length sequence before a 40-token one, sharing the block table
+        bt = t32(np.stack([wl.pre_bt, wl.pre_bt]))
+        indptr, pref = t32([0, 0, 40]), t32([0, 0])
+        out = torch.zeros_like(dw.q_pre)
+        mw.mw_prefill_attn(dw.pool, 8, 2, 128, dw.scale, [0, 40], [0, 0], indptr.data_ptr(), pref.data_ptr(),
+                           bt.data_ptr(), bt.shape[1], dw.q_pre.data_ptr(), out.data_ptr())
+        torch.cuda.synchronize()
+        ref = oracle.prefill(wl.q_pre[:40], wl.k_pool, wl.v_pool, wl.pre_bt, 0)
+        assert_close(to_bits(out[:40]), ref, "zero-length neighbour")
+    finally:
+        dw.close()
