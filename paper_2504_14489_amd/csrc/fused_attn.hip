@@ -48,7 +48,7 @@ k_fused_attn(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vp
     const int64_t p_lo = i * n_pre / total, p_hi = (i + 1) * n_pre / total;
     if (p_hi > p_lo) {
         const int x = static_cast<int>(p_lo % gx), b = static_cast<int>(p_lo / gx);
-        pf::prefill_block<kTableInLds>(kpool, vpool, pq, pout, qo_indptr, prefix_lens, pbt, pbt_stride, hkv, pgroup,
+        pf::prefill_block<kTableInLds, 8>(kpool, vpool, pq, pout, qo_indptr, prefix_lens, pbt, pbt_stride, hkv, pgroup,
                                        num_pages, pscale_log2, paired, n_hgroups, x, b,
                                        reinterpret_cast<uint16_t *>(lds + kPrefillK),
                                        reinterpret_cast<uint16_t *>(lds + kPrefillV),
@@ -74,7 +74,7 @@ extern "C" mw_status mw_fused_attn(const mw_prefill_args *pre, const mw_decode_a
     if (pre->pool != dec->pool) return fail(MW_ERR_INVALID_ARG, "%s: prefill and decode must share one pool", who);
     hipStream_t s = static_cast<hipStream_t>(stream);
     PrefillPlan pp;
-    mw_status st = prefill_prepare(pre, stream_cus(s), &pp, who);
+    mw_status st = prefill_prepare(pre, stream_cus(s), false, &pp, who);  // 8-wave work-groups only
     if (st != MW_OK) return st;
     DecodePlan dp;
     st = decode_prepare(dec, &dp, who);

@@ -90,13 +90,15 @@ mw_status decode_combine_launch(const mw_decode_args *a, const DecodePlan &p, hi
 // Checked launch parameters of one prefill call.
 struct PrefillPlan {
     int hkv, group, n_hgroups, paired;
+    int waves;            // 8 (64-position query blocks) or 4 (32-position blocks)
     int64_t gx;           // work-groups per sequence (grid x); 0: nothing to do
     int batch;
     bool table_in_lds;    // every block-table entry a work-group needs fits its LDS copy
     float scale_log2;
 };
 // Validates a prefill call's arguments and plans it for a stream that may use
-// `cus` CUs (block pairing depends on it).
-mw_status prefill_prepare(const mw_prefill_args *a, int64_t cus, PrefillPlan *p, const char *who);
+// `cus` CUs (block pairing and, with allow_small, the work-group size depend
+// on it).
+mw_status prefill_prepare(const mw_prefill_args *a, int64_t cus, bool allow_small, PrefillPlan *p, const char *who);
 
 }  // namespace mw

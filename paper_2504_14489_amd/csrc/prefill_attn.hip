@@ -8,8 +8,8 @@ namespace {
 
 using namespace pf;
 
-template <bool kTableInLds>
-__global__ void __launch_bounds__(kThreads, 1)
+template <bool kTableInLds, int NW>
+__global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1)
 k_prefill_attn(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpool,
                const uint16_t *__restrict__ q, uint16_t *__restrict__ out,
                const int32_t *__restrict__ qo_indptr, const int32_t *__restrict__ prefix_lens,
@@ -18,7 +18,7 @@ k_prefill_attn(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ 
     __shared__ __attribute__((aligned(1024))) uint16_t s_k[2 * TILE];
     __shared__ __attribute__((aligned(1024))) uint16_t s_v[2 * TILE];
     __shared__ int32_t s_bt[kBtCache];
-    prefill_block<kTableInLds>(kpool, vpool, q, out, qo_indptr, prefix_lens, bt, bt_stride, hkv, group, num_pages,
+    prefill_block<kTableInLds, NW>(kpool, vpool, q, out, qo_indptr, prefix_lens, bt, bt_stride, hkv, group, num_pages,
                                scale_log2, paired, n_hgroups, blockIdx.x, blockIdx.y, s_k, s_v, s_bt);
 }
 
@@ -26,7 +26,7 @@ k_prefill_attn(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ 
 
 namespace mw {
 
-mw_status prefill_prepare(const mw_prefill_args *a, int64_t cus, PrefillPlan *p, const char *who) {
+mw_status prefill_prepare(const mw_prefill_args *a, int64_t cus, bool allow_small, PrefillPlan *p, const char *who) {
     if (!a || !a->pool || a->batch < 0 || a->batch > 65535 || a->bt_stride < 1 ||
         (a->batch > 0 && (!a->h_new_lens || !a->h_prefix_lens)))
         return fail(MW_ERR_INVALID_ARG, "%s: bad arguments", who);
@@ -61,17 +61,29 @@ mw_status prefill_prepare(const mw_prefill_args *a, int64_t cus, PrefillPlan *p,
     p->scale_log2 = shape->scale * kLog2e;
     p->paired = 0;
     p->gx = 0;
+    p->waves = 8;
     if (max_n == 0) return MW_OK;
-    // Pair blocks only when the pairs fill whole rounds of the CUs the stream
-    // may use (one work-group fits per CU): equal-cost pairs then finish
-    // together.  Otherwise single blocks, heaviest first, fill the last round
-    // better.
-    const int64_t max_qblocks = (max_n + BM - 1) / BM;
-    int64_t n_pairs = 0;
-    for (int32_t b = 0; b < a->batch; ++b) n_pairs += ((a->h_new_lens[b] + BM - 1) / BM + 1) / 2;
-    n_pairs *= p->hkv * p->n_hgroups;
-    const int64_t rounds = (n_pairs + cus - 1) / cus;
-    p->paired = n_pairs >= cus && rounds * cus * 20 <= n_pairs * 21;
+    auto pairs_of = [&](int64_t bm) {
+        int64_t n_pairs = 0;
+        for (int32_t b = 0; b < a->batch; ++b) n_pairs += ((a->h_new_lens[b] + bm - 1) / bm + 1) / 2;
+        return n_pairs * p->hkv * p->n_hgroups;
+    };
+    // Eight waves (64-position blocks, one work-group per CU) unless their pairs
+    // would not even give every CU one: then four waves (32-position blocks,
+    // two work-groups per CU), which doubles the work-groups.
+    int64_t bm = BM, slots = cus;
+    if (allow_small && pairs_of(BM) < cus) {
+        p->waves = 4;
+        bm = BM / 2;
+        slots = 2 * cus;
+    }
+    // Pair blocks only when the pairs fill whole rounds of the work-group slots
+    // of the stream's CUs: equal-cost pairs then finish together.  Otherwise
+    // single blocks, heaviest first, fill the last round better.
+    const int64_t max_qblocks = (max_n + bm - 1) / bm;
+    const int64_t n_pairs = pairs_of(bm);
+    const int64_t rounds = (n_pairs + slots - 1) / slots;
+    p->paired = n_pairs >= slots && rounds * slots * 20 <= n_pairs * 21;
     p->gx = (p->paired ? (max_qblocks + 1) / 2 : max_qblocks) * p->hkv * p->n_hgroups;
     if (p->gx > 0x7fffffff) return fail(MW_ERR_UNSUPPORTED, "%s: grid too large", who);
     return MW_OK;
@@ -90,13 +102,14 @@ extern "C" mw_status mw_prefill_attn(const mw_kv_pool *pool, const mw_attn_shape
                             d_prefix_lens, d_block_table, bt_stride, d_q,        d_out};
     hipStream_t s = static_cast<hipStream_t>(stream);
     PrefillPlan pl;
-    mw_status st = prefill_prepare(&a, stream_cus(s), &pl, who);
+    mw_status st = prefill_prepare(&a, stream_cus(s), true, &pl, who);
     if (st != MW_OK) return st;
     st = timing_begin(timing, s);
     if (st != MW_OK) return st;
     if (pl.gx > 0) {
-        auto kernel = pl.table_in_lds ? k_prefill_attn<true> : k_prefill_attn<false>;
-        hipLaunchKernelGGL(kernel, dim3(static_cast<unsigned>(pl.gx), batch), dim3(kThreads), 0, s, pool->k,
+        auto kernel = pl.waves == 4 ? (pl.table_in_lds ? k_prefill_attn<true, 4> : k_prefill_attn<false, 4>)
+                                    : (pl.table_in_lds ? k_prefill_attn<true, 8> : k_prefill_attn<false, 8>);
+        hipLaunchKernelGGL(kernel, dim3(static_cast<unsigned>(pl.gx), batch), dim3(64 * pl.waves), 0, s, pool->k,
                            pool->v, static_cast<const uint16_t *>(d_q), static_cast<uint16_t *>(d_out), d_qo_indptr,
                            d_prefix_lens, d_block_table, bt_stride, pl.hkv, pl.group, pool->desc.num_pages,
                            pl.scale_log2, pl.paired, pl.n_hgroups);

@@ -54,7 +54,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
-constexpr int BM = 64;                       // query positions per work-group
+constexpr int BM = 64;                       // query positions per 8-wave work-group
 constexpr int BN = 64;                       // keys per tile
 constexpr int ROW = kHeadDim;                // tile row = one key, 128 bf16 (256 B)
 constexpr int TILE = BN * ROW;               // one K or V tile, bf16 elements
@@ -120,7 +120,10 @@ __device__ inline void wg_barrier() {
 // kTableInLds: every block-table entry the work-group needs fits the LDS copy.
 // The other instantiation reads entries past it with scalar loads, which makes
 // the compiler wait for all outstanding LDS reads wherever it needs one.
-template <bool kTableInLds>
+// NW: waves per work-group.  8 (query blocks of 64 positions; waves w and
+// w+4 share a SIMD) or 4 (blocks of 32 positions, two work-groups per CU):
+// the same per-wave work, for grids that would leave CUs idle with 8.
+template <bool kTableInLds, int NW>
 __device__ __forceinline__ void
 prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpool,
               const uint16_t *__restrict__ q, uint16_t *__restrict__ out,
@@ -131,6 +134,12 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
               // and the LDS buffers: K and V tiles (2 * TILE each, 1024-byte
               // aligned) and the block-table copy (kBtCache entries)
               const int x, const int b, uint16_t *s_k, uint16_t *s_v, int32_t *s_bt) {
+    static_assert(NW == 8 || NW == 4, "8 or 4 waves");
+    constexpr int kBM = 8 * NW;         // query positions per block
+    constexpr int kNT = 64 * NW;        // threads
+    constexpr int kRows = 64 / NW;      // tile rows (keys) each wave loads
+    constexpr int kJ = kRows / 4;       // 1-KB loads per wave per K (or V) tile
+    constexpr int kEvery = 8 / kJ;      // QK MFMAs between two of this wave's loads
     // Work-group = one query block of one (sequence, kv head, head group),
     // heaviest blocks first, or (paired) the pair of blocks nqb-1-i and i:
     // causal blocks grow linearly with the block index, so every pair costs
@@ -140,7 +149,7 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
     const int pair = x / (hkv * n_hgroups);
     const int row0 = qo_indptr[b];
     const int n = qo_indptr[b + 1] - row0;
-    const int nqb = (n + BM - 1) / BM;
+    const int nqb = (n + kBM - 1) / kBM;
     if (pair >= (paired ? (nqb + 1) / 2 : nqb)) return;
     const int n_items = (!paired || pair == nqb - 1 - pair) ? 1 : 2;
     const int r = prefix_lens[b];
@@ -157,9 +166,9 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
 
     // block-table entries of this work-group's keys (the heavier block's)
     {
-        const int nt_a = (r + min((nqb - pair) * BM, n) + BN - 1) / BN;
+        const int nt_a = (r + min((nqb - pair) * kBM, n) + BN - 1) / BN;
         const int np_wg = min(4 * nt_a, np_seq);
-        for (int i = threadIdx.x; i < min(np_wg, kBtCache); i += kThreads) s_bt[i] = btrow[i];
+        for (int i = threadIdx.x; i < min(np_wg, kBtCache); i += kNT) s_bt[i] = btrow[i];
     }
     const int first_page = btrow[0];
     const int safe_page = (first_page >= 0 && first_page < num_pages) ? first_page : 0;
@@ -181,16 +190,16 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
             voff[hh] = row * 256 + 16 * chunk + 8 * (s16 & 1);
         }
     }
-    // direct loads: wave w moves rows 8w + 4j + lane/16 (j = 0, 1) of every K
-    // and V tile, all in page w/2 of the tile; lane i lands in physical chunk
-    // i%16.  Byte offsets within the page:
-    int goff[2];
+    // direct loads: wave w moves rows kRows w + 4j + lane/16 (j < kJ) of every
+    // K and V tile, all in page kRows w / 16 of the tile; lane i lands in
+    // physical chunk i%16.  Byte offsets within the page:
+    int goff[kJ];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-        const int row = 8 * (wave & 1) + 4 * j + (lane >> 4);
+    for (int j = 0; j < kJ; ++j) {
+        const int row = (kRows * wave) % 16 + 4 * j + (lane >> 4);
         goff[j] = 2 * (row * kHeadDim + 8 * ((lane & 15) ^ swz(row)));
     }
-    const int lpage = wave >> 1;  // page of the tile this wave loads
+    const int lpage = kRows * wave / 16;  // page of the tile this wave loads
 
     // per-item state
     int qblk = 0, nt = 0, pos = 0, qabs = 0, diag = 0;
@@ -230,7 +239,7 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
     };
     auto page_load = [&](__amdgpu_buffer_rsrc_t rsrc, uint16_t *dst, int j) __attribute__((always_inline)) {
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            rsrc, reinterpret_cast<lds_void *>(reinterpret_cast<uintptr_t>(dst + (8 * wave + 4 * j) * ROW)), 16,
+            rsrc, reinterpret_cast<lds_void *>(reinterpret_cast<uintptr_t>(dst + (kRows * wave + 4 * j) * ROW)), 16,
             goff[j], 0, 0, 0);
     };
 
@@ -283,7 +292,7 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
                     a, __builtin_bit_cast(bf16x8, qop[j >> 1]), sacc[j & 1], 0, 0, 0);
             }
             if (i + kAhead < nop) opnd[i % kAhead] = fetch(i + kAhead);
-            if ((i & 3) == 3) load(i >> 2);
+            if (!PV && i % kEvery == kEvery - 1) load(i / kEvery);
             __builtin_amdgcn_sched_barrier(0);
         }
         __builtin_amdgcn_s_setprio(0);
@@ -344,7 +353,7 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
         const size_t base = page_base(p < np_seq ? btrow[p] : -1);
         const __amdgpu_buffer_rsrc_t rk = page_rsrc(kpool, base), rv = page_rsrc(vpool, base);
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
+        for (int j = 0; j < kJ; ++j) {
             page_load(rk, s_k, j);
             page_load(rv, s_v, j);
         }
@@ -352,10 +361,10 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
 
     for (int item = 0; item < n_items; ++item) {
         qblk = item == 0 ? nqb - 1 - pair : pair;
-        nt = (r + min(qblk * BM + BM, n) + BN - 1) / BN;
-        pos = qblk * BM + (wave >> 2) * 32 + l32;  // this lane's query column
+        nt = (r + min(qblk * kBM + kBM, n) + BN - 1) / BN;
+        pos = qblk * kBM + (wave >> 2) * 32 + l32;  // this lane's query column
         qabs = r + pos;
-        diag = r + qblk * BM + (wave >> 2) * 32;  // smallest query of the wave
+        diag = r + qblk * kBM + (wave >> 2) * 32;  // smallest query of the wave
         if (item > 0) wg_barrier();  // the previous item's output staging is done
         first_tile();
         // Q^T operand, all 8 dim-steps (k = 16*kb + 8*g + e)
@@ -386,10 +395,10 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
             uint16_t *dv = s_v + ((t + 1) & 1) * TILE;
             auto load = [&](int j) __attribute__((always_inline)) {
                 if (more) {
-                    if (j < 2)
+                    if (j < kJ)
                         page_load(rk, dk, j);
                     else
-                        page_load(rv, dv, j - 2);
+                        page_load(rv, dv, j - kJ);
                 }
             };
             if (active) {
@@ -398,7 +407,7 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
                 mfma_phase(flag<true>(), flag<false>(), t, [](int) {});
             } else {
 #pragma unroll
-                for (int j = 0; j < 4; ++j) load(j);
+                for (int j = 0; j < 2 * kJ; ++j) load(j);
             }
             __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's direct loads landed
             wg_barrier();
@@ -426,7 +435,7 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
             for (int j = 0; j < 8; ++j) {
                 const int row = 4 * j + (lane >> 4), c = lane & 15;
                 const uint4 v = *reinterpret_cast<const uint4 *>(st + row * 256 + 16 * (c ^ (row & 15)));
-                const int prow = qblk * BM + (wave >> 2) * 32 + row;
+                const int prow = qblk * kBM + (wave >> 2) * 32 + row;
                 if (prow < n)
                     *reinterpret_cast<uint4 *>(out + (static_cast<size_t>(row0 + prow) * hq + h) * kHeadDim + 8 * c) = v;
             }

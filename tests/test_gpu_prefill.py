@@ -123,7 +123,10 @@ def test_prefill_varlen_batch():
 
 def test_prefill_same_result_on_any_cu_count():
     """The launch pairs heavy and light query blocks only when the pairs fill
-    whole rounds of the stream's CUs; either split must give the same bits."""
+    whole rounds of the stream's CUs, and uses 4-wave work-groups on 32-position
+    blocks when the 8-wave pairs would not give every CU one (here: paired
+    8-wave blocks on 32 CUs, single 4-wave blocks on 64 and on all CUs); every
+    split must give the same bits."""
     say("prefill split independence (32 / 64 / all CUs)")
     from paper_2504_14489_amd.device import Partition
     cfg = W.custom_config(hq=32, hkv=8, pre_chunks=((0, 512),), dec_batch=1, dec_len_lo=1,
