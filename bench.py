@@ -238,7 +238,7 @@ class Bench:
 
 
 KERNEL_SOURCES = {"k_prefill_attn": ("prefill_attn.hip", "prefill_block.h"),
-                  "k_decode_split": ("decode_attn.hip", "decode_block.h")}
+                  "k_decode_balanced": ("decode_attn.hip", "decode_block.h")}
 
 
 def source_sha(kernel):
@@ -438,7 +438,7 @@ def roofline_entries(b, res):
     pre["frac"] = pre["achieved"] / pre["peak"]
     pre["share_peak"] = BF16_PEAK_TFLOPS * res["prefill_cus"] / N_CU
     pre["frac_share"] = pre["achieved"] / pre["share_peak"]
-    dec = {"kernel": "k_decode_split", "bound": "hbm", "unit": "GB/s",
+    dec = {"kernel": "k_decode_balanced", "bound": "hbm", "unit": "GB/s",
            "achieved": b.dec_bytes / (dec_ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
            "work_per_launch": b.dec_bytes, "kernel_ms": dec_ms}
     dec["frac"] = dec["achieved"] / dec["peak"]

@@ -230,12 +230,21 @@ mw_status mw_prefill_attn(const mw_kv_pool *pool, const mw_attn_shape *shape, in
                           const int32_t *d_block_table, int32_t bt_stride, const void *d_q,
                           void *d_out, mw_stream stream, mw_timing *timing);
 
-/* Decode is split over chunks of `chunk_pages` pages of each sequence (a
- * multiple of 8 in [8, 256]; 0 = chosen from the lengths: the largest of 128,
- * 64 and 32 that still gives at least 1024 (chunk, kv head) work units) and
- * merged by a second kernel (log-sum-exp combine).  The split depends only on
- * the lengths, never on page ids; pass the same chunk_pages (and lengths) to
- * both calls.
+/* Decode streams each (sequence, kv head) segment of the K/V pages split into
+ * pieces whose partial results a second kernel merges (log-sum-exp combine,
+ * the flash-decoding split of Sec. 2.2's memory-bound decode).  chunk_pages
+ * chooses the split:
+ *   0  (default) balanced: the segments laid end to end are cut into equal
+ *      ranges of pages, two per CU of the stream the call runs on (at most
+ *      512, at least 8 pages each); a range may cross segment boundaries and
+ *      every CU streams the same number of bytes.  The split depends on the
+ *      lengths and on the stream's CU count.
+ *   -1 fixed chunks chosen from the lengths: the largest of 128, 64 and 32
+ *      pages that still gives at least 1024 (chunk, kv head) work units.
+ *   8..256, a multiple of 8: fixed chunks of that many pages.
+ * No split ever depends on page ids (renumbering pages changes no result).
+ * Pass the same chunk_pages (and lengths) to both calls; the size for 0
+ * covers both splits that chunk_pages 0 can select (see mw_fused_attn).
  * Workspace bytes for a call with these lengths: */
 mw_status mw_decode_workspace_size(const mw_attn_shape *shape, int32_t batch,
                                    const int32_t *h_seq_lens, int32_t chunk_pages,
@@ -431,8 +440,12 @@ typedef struct {
  * their counts, then the decode combine kernel runs.  Arguments, layouts and
  * results are those of mw_prefill_attn (pre) and mw_decode_attn (dec) with
  * the same checks; both must name the same pool, and the prefill outputs must
- * not overlap the decode outputs or workspace.  Outputs are bit-identical to
- * the two separate calls.  timing records 2 kernels (fused, combine). */
+ * not overlap the decode outputs or workspace.  The decode work units are
+ * fixed chunks (dec->chunk_pages 0 is taken as -1: the balanced split's
+ * units differ in their number of work-group barriers, which the two halves
+ * of a fused work-group cannot).  Outputs are bit-identical to the two
+ * separate calls with the same chunks.  timing records 2 kernels (fused,
+ * combine). */
 mw_status mw_fused_attn(const mw_prefill_args *pre, const mw_decode_args *dec, mw_stream stream,
                         mw_timing *timing);
 

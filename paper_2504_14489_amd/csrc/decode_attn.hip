@@ -1,6 +1,8 @@
 // Decode attention: one query token per sequence over its paged context --
 // the split kernel (its work-unit body is in decode_block.h), the combine
 // kernel and their launch.
+#include <algorithm>
+
 #include "decode_block.h"
 
 using namespace mw;
@@ -22,20 +24,53 @@ k_decode_split(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ 
                        num_pages, scale_log2, ch_pages, blockIdx.x, threadIdx.x, s_v, s_m, s_l);
 }
 
+// Balanced split: unit u streams pages [u per_unit, (u + 1) per_unit) of the
+// batch's (sequence, kv head) segments laid end to end.
+__global__ void __launch_bounds__(kThreads)
+k_decode_balanced(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpool,
+                  const uint16_t *__restrict__ q, uint16_t *__restrict__ out,
+                  const int32_t *__restrict__ seq_lens, const int32_t *__restrict__ bt, int bt_stride,
+                  float *__restrict__ ws_o, float2 *__restrict__ ws_ml, int32_t *__restrict__ ws_cbase,
+                  int batch, int hkv, int group, int num_pages, float scale_log2, int64_t per_unit,
+                  int64_t total) {
+    __shared__ __attribute__((aligned(16))) uint16_t s_v[kWaves * kVBufElems];
+    __shared__ float s_m[kWaves][16];
+    __shared__ float s_l[kWaves][16];
+    decode_span(kpool, vpool, q, out, seq_lens, bt, bt_stride, ws_o, ws_ml, ws_cbase, batch, hkv, group, num_pages,
+                scale_log2, per_unit, total, blockIdx.x, threadIdx.x, s_v, s_m, s_l);
+}
+
 // One work-group per (sequence, kv head); thread pairs (h, d).  The partials
-// of all chunks are loaded with independent loads (8 chunks in flight).
+// of the segment's pieces are loaded with independent loads (8 in flight).
+// Fixed chunks (per_unit = 0): chunk c of sequence b is slot
+// (ws_cbase[b] + c) hkv + kv head.  Balanced split (per_unit > 0): the
+// segment starts at global page P = ws_cbase[b] + kv head * pages(b), and its
+// pieces are those of units P / per_unit .. (P + pages(b) - 1) / per_unit,
+// unit u's piece in slot u + b hkv + kv head.
 __global__ void __launch_bounds__(kThreads)
 k_decode_combine(uint16_t *__restrict__ out, const int32_t *__restrict__ seq_lens,
                  const float *__restrict__ ws_o, const float2 *__restrict__ ws_ml,
                  const int32_t *__restrict__ ws_cbase, int hkv, int group, int ch_pages, int bt_stride,
-                 int total_chunks) {
+                 int64_t per_unit, int64_t slots) {
     const int b = blockIdx.x / hkv, kvh = blockIdx.x % hkv;
-    const int nch = chunks_of(seq_lens[b], ch_pages, bt_stride);
+    int64_t first = 0, stride = hkv;  // slot of piece j: first + j * stride
+    int nch = 0;
+    if (per_unit > 0) {
+        const int np = chunks_of(seq_lens[b], 1, bt_stride);
+        const int64_t start = static_cast<int64_t>(ws_cbase[b]) + static_cast<int64_t>(kvh) * np;
+        if (np <= 0 || start < 0) return;
+        const int64_t u0 = start / per_unit, u1 = (start + np - 1) / per_unit;
+        nch = static_cast<int>(u1 - u0 + 1);
+        first = u0 + static_cast<int64_t>(b) * hkv + kvh;
+        stride = 1;
+    } else {
+        nch = chunks_of(seq_lens[b], ch_pages, bt_stride);
+        first = static_cast<int64_t>(ws_cbase[b]) * hkv + kvh;
+    }
     if (nch <= 1) return;  // written by the split kernel
-    const int cbase = ws_cbase[b];
     // lengths on the device that disagree with the host copy must not lead
     // outside the workspace
-    if (cbase < 0 || cbase + nch > total_chunks) return;
+    if (first < 0 || first + static_cast<int64_t>(nch - 1) * stride >= slots) return;
     const int hq = hkv * group;
     for (int idx = threadIdx.x; idx < group * kHeadDim; idx += kThreads) {
         const int h = idx / kHeadDim, d = idx % kHeadDim;
@@ -44,7 +79,7 @@ k_decode_combine(uint16_t *__restrict__ out, const int32_t *__restrict__ seq_len
             float2 ml[8];
 #pragma unroll
             for (int j = 0; j < 8; ++j)
-                ml[j] = s0 + j < nch ? ws_ml[(static_cast<size_t>(cbase + s0 + j) * hkv + kvh) * group + h]
+                ml[j] = s0 + j < nch ? ws_ml[static_cast<size_t>(first + (s0 + j) * stride) * group + h]
                                      : make_float2(-INFINITY, 0.f);
 #pragma unroll
             for (int j = 0; j < 8; ++j)
@@ -56,7 +91,7 @@ k_decode_combine(uint16_t *__restrict__ out, const int32_t *__restrict__ seq_len
             float o[8];
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
-                const size_t uu = (static_cast<size_t>(cbase + s0 + j) * hkv + kvh) * group + h;
+                const size_t uu = static_cast<size_t>(first + (s0 + j) * stride) * group + h;
                 const bool in = s0 + j < nch;
                 ml[j] = in ? ws_ml[uu] : make_float2(-INFINITY, 0.f);
                 o[j] = in ? ws_o[uu * kHeadDim + d] : 0.f;
@@ -73,16 +108,36 @@ k_decode_combine(uint16_t *__restrict__ out, const int32_t *__restrict__ seq_len
     }
 }
 
+// Balanced split: units per CU of the stream (two 4-wave work-groups fit a
+// CU), the most units (two per CU of a 256-CU device; the workspace is sized
+// for it) and the fewest pages a unit streams (one pair per wave).
+constexpr int64_t kBalancedPerCu = 2;
+constexpr int64_t kBalancedMaxUnits = 512;
+constexpr int64_t kBalancedMinPages = 8;
+
 struct Plan {
-    int64_t units;
-    int chunk_pages;
+    int64_t units;            // work-groups of the split kernel
+    int chunk_pages;          // fixed chunks; 0 with the balanced split
+    int64_t per_unit, total;  // balanced split: pages per unit, pages in all
+    int64_t slots;            // partial slots of the workspace
     size_t off_ml, off_cbase, bytes;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
+void plan_layout(Plan *plan, int32_t batch, int group) {
+    const size_t o_bytes = align256(static_cast<size_t>(plan->slots) * group * kHeadDim * 4);
+    const size_t ml_bytes = align256(static_cast<size_t>(plan->slots) * group * 8);
+    plan->off_ml = o_bytes;
+    plan->off_cbase = o_bytes + ml_bytes;
+    plan->bytes = plan->off_cbase + align256(static_cast<size_t>(batch) * 4 + 4);
+}
+
+// chunk_pages > 0: fixed chunks of that many pages; -1 (or 0 with cus = 0):
+// automatic fixed chunks; 0 with cus > 0: the balanced split over cus CUs
+// (cus < 0: the largest balanced split, for sizing a workspace).
 mw_status plan_decode(const mw_attn_shape *shape, int32_t batch, const int32_t *h_seq_lens,
-                      int32_t chunk_pages, int32_t bt_stride, Plan *plan, const char *who) {
+                      int32_t chunk_pages, int32_t bt_stride, int64_t cus, Plan *plan, const char *who) {
     if (!shape || batch < 0 || (batch > 0 && !h_seq_lens))
         return fail(MW_ERR_INVALID_ARG, "%s: bad arguments", who);
     if (shape->head_dim != kHeadDim) return fail(MW_ERR_UNSUPPORTED, "%s: head_dim must be 128", who);
@@ -90,8 +145,8 @@ mw_status plan_decode(const mw_attn_shape *shape, int32_t batch, const int32_t *
         return fail(MW_ERR_INVALID_ARG, "%s: num_q_heads must be a positive multiple of num_kv_heads", who);
     if (shape->num_q_heads / shape->num_kv_heads > 16)
         return fail(MW_ERR_UNSUPPORTED, "%s: at most 16 query heads per kv head", who);
-    if (chunk_pages != 0 && (chunk_pages < 8 || chunk_pages > 256 || chunk_pages % 8))
-        return fail(MW_ERR_UNSUPPORTED, "%s: chunk_pages must be a multiple of 8 in [8, 256] (or 0)", who);
+    if (chunk_pages != 0 && chunk_pages != -1 && (chunk_pages < 8 || chunk_pages > 256 || chunk_pages % 8))
+        return fail(MW_ERR_UNSUPPORTED, "%s: chunk_pages must be a multiple of 8 in [8, 256] (or 0, -1)", who);
     for (int32_t b = 0; b < batch; ++b) {
         const int32_t L = h_seq_lens[b];
         if (L < 1 || (bt_stride > 0 && static_cast<int64_t>(L) > static_cast<int64_t>(bt_stride) * kPageSize))
@@ -103,23 +158,44 @@ mw_status plan_decode(const mw_attn_shape *shape, int32_t batch, const int32_t *
         for (int32_t b = 0; b < batch; ++b) n += ((h_seq_lens[b] + kPageSize - 1) / kPageSize + ch - 1) / ch;
         return n;
     };
-    if (chunk_pages == 0) {
-        chunk_pages = kAutoChunks[2];
-        for (int ch : kAutoChunks)
-            if (count(ch) * shape->num_kv_heads >= kAutoMinUnits) {
-                chunk_pages = ch;
-                break;
-            }
-    }
-    plan->chunk_pages = chunk_pages;
-    const int64_t chunks = count(chunk_pages);
     const int group = shape->num_q_heads / shape->num_kv_heads;
-    plan->units = chunks * shape->num_kv_heads;
-    const size_t o_bytes = align256(static_cast<size_t>(plan->units) * group * kHeadDim * 4);
-    const size_t ml_bytes = align256(static_cast<size_t>(plan->units) * group * 8);
-    plan->off_ml = o_bytes;
-    plan->off_cbase = o_bytes + ml_bytes;
-    plan->bytes = plan->off_cbase + align256(static_cast<size_t>(batch) * 4 + 4);
+    const int64_t hkv = shape->num_kv_heads;
+    auto fixed = [&](int ch, Plan *pl) {
+        if (ch <= 0) {
+            ch = kAutoChunks[2];
+            for (int c : kAutoChunks)
+                if (count(c) * hkv >= kAutoMinUnits) {
+                    ch = c;
+                    break;
+                }
+        }
+        pl->chunk_pages = ch;
+        pl->units = pl->slots = count(ch) * hkv;
+        pl->per_unit = pl->total = 0;
+        plan_layout(pl, batch, group);
+    };
+    auto balanced = [&](int64_t n_cus, Plan *pl) {
+        pl->chunk_pages = 0;
+        pl->total = count(1) * hkv;
+        int64_t units = std::min(kBalancedPerCu * std::max<int64_t>(n_cus, 1), kBalancedMaxUnits);
+        units = std::max<int64_t>(1, std::min(units, (pl->total + kBalancedMinPages - 1) / kBalancedMinPages));
+        pl->per_unit = std::max<int64_t>(1, (pl->total + units - 1) / units);
+        pl->units = pl->total > 0 ? (pl->total + pl->per_unit - 1) / pl->per_unit : 0;
+        // piece of unit u of segment s in slot u + s
+        pl->slots = pl->units > 0 ? pl->units + static_cast<int64_t>(batch) * hkv - 1 : 0;
+        plan_layout(pl, batch, group);
+    };
+    if (chunk_pages == 0 && cus < 0) {
+        // workspace for either split of chunk_pages = 0
+        Plan a, b;
+        fixed(0, &a);
+        balanced(kBalancedMaxUnits, &b);
+        *plan = a.bytes >= b.bytes ? a : b;
+    } else if (chunk_pages == 0 && cus > 0) {
+        balanced(cus, plan);
+    } else {
+        fixed(chunk_pages, plan);
+    }
     return MW_OK;
 }
 
@@ -127,11 +203,11 @@ mw_status plan_decode(const mw_attn_shape *shape, int32_t batch, const int32_t *
 
 namespace mw {
 
-mw_status decode_prepare(const mw_decode_args *a, DecodePlan *p, const char *who) {
+mw_status decode_prepare(const mw_decode_args *a, int64_t cus, DecodePlan *p, const char *who) {
     if (!a || !a->pool || a->bt_stride < 1) return fail(MW_ERR_INVALID_ARG, "%s: bad pool or bt_stride", who);
     const mw_attn_shape *shape = &a->shape;
     Plan pl;
-    mw_status st = plan_decode(shape, a->batch, a->h_seq_lens, a->chunk_pages, a->bt_stride, &pl, who);
+    mw_status st = plan_decode(shape, a->batch, a->h_seq_lens, a->chunk_pages, a->bt_stride, cus, &pl, who);
     if (st != MW_OK) return st;
     if (!(shape->scale > 0.f) || !(shape->scale < INFINITY))
         return fail(MW_ERR_INVALID_ARG, "%s: scale must be positive and finite", who);
@@ -145,8 +221,13 @@ mw_status decode_prepare(const mw_decode_args *a, DecodePlan *p, const char *who
     if (a->workspace_bytes < pl.bytes)
         return fail(MW_ERR_INVALID_ARG, "%s: workspace of %zu bytes, %zu needed", who, a->workspace_bytes, pl.bytes);
     if (pl.units > 0x7fffffff) return fail(MW_ERR_UNSUPPORTED, "%s: too many work units", who);
+    if (pl.per_unit > 0 && pl.total + pl.units > 0x7fffffff)
+        return fail(MW_ERR_UNSUPPORTED, "%s: too many pages for the balanced split", who);
     p->units = pl.units;
     p->chunk_pages = pl.chunk_pages;
+    p->per_unit = pl.per_unit;
+    p->total = pl.total;
+    p->slots = pl.slots;
     p->off_ml = pl.off_ml;
     p->off_cbase = pl.off_cbase;
     p->bytes = pl.bytes;
@@ -163,7 +244,7 @@ mw_status decode_combine_launch(const mw_decode_args *a, const DecodePlan &p, hi
                        static_cast<uint16_t *>(a->d_out), a->d_seq_lens, reinterpret_cast<const float *>(ws),
                        reinterpret_cast<const float2 *>(ws + p.off_ml),
                        reinterpret_cast<const int32_t *>(ws + p.off_cbase), p.hkv, p.group, p.chunk_pages,
-                       a->bt_stride, static_cast<int>(p.units / p.hkv));
+                       a->bt_stride, p.per_unit, p.slots);
     return check_launch("k_decode_combine");
 }
 
@@ -175,7 +256,7 @@ mw_status mw_decode_workspace_size(const mw_attn_shape *shape, int32_t batch, co
                                    int32_t chunk_pages, size_t *bytes) {
     if (!bytes) return fail(MW_ERR_INVALID_ARG, "mw_decode_workspace_size: bytes is NULL");
     Plan pl;
-    mw_status st = plan_decode(shape, batch, h_seq_lens, chunk_pages, 0, &pl, "mw_decode_workspace_size");
+    mw_status st = plan_decode(shape, batch, h_seq_lens, chunk_pages, 0, -1, &pl, "mw_decode_workspace_size");
     if (st != MW_OK) return st;
     *bytes = pl.bytes;
     return MW_OK;
@@ -189,20 +270,31 @@ mw_status mw_decode_attn(const mw_kv_pool *pool, const mw_attn_shape *shape, int
     if (!shape) return fail(MW_ERR_INVALID_ARG, "%s: bad arguments", who);
     const mw_decode_args a{pool,   *shape, batch,        h_seq_lens,      d_seq_lens, d_block_table,
                            bt_stride, d_q, d_out, d_workspace, workspace_bytes, chunk_pages};
-    DecodePlan pl;
-    mw_status st = decode_prepare(&a, &pl, who);
-    if (st != MW_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
+    DecodePlan pl;
+    mw_status st = decode_prepare(&a, stream_cus(s), &pl, who);
+    if (st != MW_OK) return st;
     st = timing_begin(timing, s);
     if (st != MW_OK) return st;
     if (pl.units > 0) {
         char *ws = static_cast<char *>(d_workspace);
-        hipLaunchKernelGGL(k_decode_split, dim3(static_cast<unsigned>(pl.units)), dim3(kThreads), 0, s, pool->k,
-                           pool->v, static_cast<const uint16_t *>(d_q), static_cast<uint16_t *>(d_out), d_seq_lens,
-                           d_block_table, bt_stride, reinterpret_cast<float *>(ws),
-                           reinterpret_cast<float2 *>(ws + pl.off_ml), reinterpret_cast<int32_t *>(ws + pl.off_cbase),
-                           batch, pl.hkv, pl.group, pool->desc.num_pages, pl.scale_log2, pl.chunk_pages);
-        st = check_launch("k_decode_split");
+        if (pl.per_unit > 0) {
+            hipLaunchKernelGGL(k_decode_balanced, dim3(static_cast<unsigned>(pl.units)), dim3(kThreads), 0, s,
+                               pool->k, pool->v, static_cast<const uint16_t *>(d_q), static_cast<uint16_t *>(d_out),
+                               d_seq_lens, d_block_table, bt_stride, reinterpret_cast<float *>(ws),
+                               reinterpret_cast<float2 *>(ws + pl.off_ml),
+                               reinterpret_cast<int32_t *>(ws + pl.off_cbase), batch, pl.hkv, pl.group,
+                               pool->desc.num_pages, pl.scale_log2, pl.per_unit, pl.total);
+            st = check_launch("k_decode_balanced");
+        } else {
+            hipLaunchKernelGGL(k_decode_split, dim3(static_cast<unsigned>(pl.units)), dim3(kThreads), 0, s,
+                               pool->k, pool->v, static_cast<const uint16_t *>(d_q), static_cast<uint16_t *>(d_out),
+                               d_seq_lens, d_block_table, bt_stride, reinterpret_cast<float *>(ws),
+                               reinterpret_cast<float2 *>(ws + pl.off_ml),
+                               reinterpret_cast<int32_t *>(ws + pl.off_cbase), batch, pl.hkv, pl.group,
+                               pool->desc.num_pages, pl.scale_log2, pl.chunk_pages);
+            st = check_launch("k_decode_split");
+        }
         if (st != MW_OK) return st;
     }
     st = timing_kernel_done(timing, s);

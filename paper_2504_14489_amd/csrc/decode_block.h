@@ -132,34 +132,21 @@ __device__ inline void pair_load(PairRegs &pr, const uint16_t *__restrict__ kpoo
     }
 }
 
-// One (sequence, kv head, chunk) work unit on 4 waves.  tid = thread index
-// within the 4 waves (0..255); s_v, s_m, s_l are those waves' LDS.
-// kGuarded: the caller runs other work in the same work-group, so a unit
-// past the end does nothing but still takes the two work-group barriers.
-template <bool kGuarded>
+// Pages [p_begin, p_end) of sequence b (length L, block-table row btrow),
+// kv head kvh, on 4 waves; tid = thread index within them (0..255); s_v,
+// s_m, s_l are their LDS.  The merged result is written as the bf16 output
+// (direct) or as the fp32 partial (O, (m, l)) of workspace slot `slot`.
+// active = false (uniform): nothing is read or written, but both work-group
+// barriers are still taken.
 __device__ __forceinline__ void
-decode_unit(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpool,
-               const uint16_t *__restrict__ q, uint16_t *__restrict__ out,
-               const int32_t *__restrict__ seq_lens, const int32_t *__restrict__ bt, int bt_stride,
-               float *__restrict__ ws_o, float2 *__restrict__ ws_ml, int32_t *__restrict__ ws_cbase,
-               int batch, int hkv, int group, int num_pages, float scale_log2, int ch_pages,
-            int u, int tid, uint16_t *s_v, float (*s_m)[16], float (*s_l)[16]) {
-
-    const int kvh = u % hkv;
-    int b = 0, c = 0, nch = 0, first = 0;
-    const bool found = locate_chunk(seq_lens, batch, ch_pages, bt_stride, u / hkv, b, c, nch, first);
-    // more units than the device lengths give (uniform over the 4 waves): a
-    // kernel of its own returns; a fused work-group still takes both barriers
-    if constexpr (!kGuarded) {
-        if (!found) return;
-    }
-
+decode_pages(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpool,
+             const uint16_t *__restrict__ q, uint16_t *__restrict__ out, const int32_t *__restrict__ btrow,
+             float *__restrict__ ws_o, float2 *__restrict__ ws_ml, int b, int L, int hkv, int kvh, int group,
+             int num_pages, float scale_log2, int p_begin, int p_end, bool active, bool direct, int64_t slot,
+             int tid, uint16_t *s_v, float (*s_m)[16], float (*s_l)[16]) {
     const int lane = tid & 63, wave = tid >> 6;
     const int col = lane & 15, grp = lane >> 4;
-    const int L = min(seq_lens[b], bt_stride * kPageSize);
-    const int np_b = (L + kPageSize - 1) / kPageSize;
-    const int p_end = found ? min((c + 1) * ch_pages, np_b) : 0;
-    const int32_t *btrow = bt + static_cast<size_t>(b) * bt_stride;
+    if (!active) p_end = p_begin;
     const int hq = hkv * group;
 
     // Q^T operand: column `col` is query head kvh*group + col
@@ -182,8 +169,8 @@ decode_unit(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpo
     // the second page), dims 4(s%4) (+16 db)
     const uint16_t *vtr = vbuf + (4 * grp + (col >> 2)) * VSTR + 4 * (col & 3);
 
-    // this wave's pairs: pages c*CH + 2*(wave + 4*j) + {0, 1}
-    const int pstart = c * ch_pages + kPair * wave;
+    // this wave's pairs: pages p_begin + 2*(wave + 4*j) + {0, 1}
+    const int pstart = p_begin + kPair * wave;
     const int pstep = kPair * kWaves;
     PairRegs pr;
     if (pstart < p_end) pair_load(pr, kpool, vpool, btrow, pstart, p_end, hkv, kvh, num_pages);
@@ -270,7 +257,7 @@ decode_unit(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpo
 #pragma unroll
         for (int i = 0; i < 4; ++i) s_o[(wave * kHeadDim + 16 * db + 4 * grp + i) * 16 + col] = oacc[db][i];
     __syncthreads();
-    for (int idx = tid; found && idx < group * kHeadDim; idx += kThreads) {
+    for (int idx = tid; active && idx < group * kHeadDim; idx += kThreads) {
         const int h = idx / kHeadDim, d = idx % kHeadDim;
         float M = -INFINITY;
 #pragma unroll
@@ -283,14 +270,114 @@ decode_unit(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpo
             lsum += wt * s_l[w][h];
             o += wt * s_o[(w * kHeadDim + d) * 16 + h];
         }
-        if (nch == 1) {
+        if (direct) {
             out[(static_cast<size_t>(b) * hq + kvh * group + h) * kHeadDim + d] = to_bf16(o / lsum);
         } else {
-            ws_o[(static_cast<size_t>(u) * group + h) * kHeadDim + d] = o;
-            if (d == 0) ws_ml[static_cast<size_t>(u) * group + h] = make_float2(M, lsum);
+            ws_o[(static_cast<size_t>(slot) * group + h) * kHeadDim + d] = o;
+            if (d == 0) ws_ml[static_cast<size_t>(slot) * group + h] = make_float2(M, lsum);
         }
     }
+}
+
+// One (sequence, kv head, chunk) work unit of the fixed-chunk split: unit u
+// is chunk u / hkv of the batch's chunks in order, kv head u % hkv.  A
+// sequence of one chunk is written directly; otherwise the chunk's partial
+// goes to slot u and the sequence's first chunk index to ws_cbase[b].
+// kGuarded: the caller runs other work in the same work-group, so a unit
+// past the end does nothing but still takes the two work-group barriers.
+template <bool kGuarded>
+__device__ __forceinline__ void
+decode_unit(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpool,
+            const uint16_t *__restrict__ q, uint16_t *__restrict__ out, const int32_t *__restrict__ seq_lens,
+            const int32_t *__restrict__ bt, int bt_stride, float *__restrict__ ws_o, float2 *__restrict__ ws_ml,
+            int32_t *__restrict__ ws_cbase, int batch, int hkv, int group, int num_pages, float scale_log2,
+            int ch_pages, int u, int tid, uint16_t *s_v, float (*s_m)[16], float (*s_l)[16]) {
+    const int kvh = u % hkv;
+    int b = 0, c = 0, nch = 0, first = 0;
+    const bool found = locate_chunk(seq_lens, batch, ch_pages, bt_stride, u / hkv, b, c, nch, first);
+    // more units than the device lengths give (uniform over the 4 waves): a
+    // kernel of its own returns; a fused work-group still takes both barriers
+    if constexpr (!kGuarded) {
+        if (!found) return;
+    }
+    const int L = min(seq_lens[b], bt_stride * kPageSize);
+    const int np_b = (L + kPageSize - 1) / kPageSize;
+    decode_pages(kpool, vpool, q, out, bt + static_cast<size_t>(b) * bt_stride, ws_o, ws_ml, b, L, hkv, kvh,
+                 group, num_pages, scale_log2, c * ch_pages, min((c + 1) * ch_pages, np_b), found, nch == 1, u,
+                 tid, s_v, s_m, s_l);
     if (found && c == 0 && kvh == 0 && tid == 0) ws_cbase[b] = first;
+}
+
+// Wave-level search for the sequence b whose kv-head segments hold global
+// page g of the balanced split (segments in the order (b, kv head), each of
+// the sequence's page count); base_out = hkv * (pages of sequences < b).
+// Returns false if g is past the end.
+__device__ bool locate_page(const int32_t *__restrict__ seq_lens, int batch, int bt_stride, int hkv, int64_t g,
+                            int &b_out, int64_t &base_out) {
+    const int lane = threadIdx.x & 63;
+    int64_t running = 0;
+    for (int base = 0; base < batch; base += 64) {
+        const int bb = base + lane;
+        const int64_t n = bb < batch ? static_cast<int64_t>(hkv) * chunks_of(seq_lens[bb], 1, bt_stride) : 0;
+        int64_t x = n;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int64_t y = __shfl_up(x, off);
+            if (lane >= off) x += y;
+        }
+        const int64_t incl = running + x, excl = incl - n;
+        const uint64_t hit = __builtin_amdgcn_ballot_w64(bb < batch && g >= excl && g < incl);
+        if (hit) {
+            const int src = __builtin_ctzll(hit);
+            base_out = __shfl(excl, src);
+            b_out = base + src;
+            return true;
+        }
+        running = __shfl(incl, 63);
+    }
+    return false;
+}
+
+// One unit of the balanced split: global pages [u R, min((u + 1) R, total))
+// of the (sequence, kv head) segments in order, which may cross segment
+// boundaries.  Each segment piece is merged on its own: a segment the unit
+// holds whole is written directly, a piece of a longer segment goes to slot
+// u + s (s = b hkv + kv head), and the unit that starts sequence b writes
+// hkv * (pages of sequences < b) to ws_cbase[b] for the combine kernel.
+// Not for fused work-groups: the number of barriers depends on the unit.
+__device__ __forceinline__ void
+decode_span(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpool,
+            const uint16_t *__restrict__ q, uint16_t *__restrict__ out, const int32_t *__restrict__ seq_lens,
+            const int32_t *__restrict__ bt, int bt_stride, float *__restrict__ ws_o, float2 *__restrict__ ws_ml,
+            int32_t *__restrict__ ws_cbase, int batch, int hkv, int group, int num_pages, float scale_log2,
+            int64_t per_unit, int64_t total, int u, int tid, uint16_t *s_v, float (*s_m)[16], float (*s_l)[16]) {
+    int64_t g = static_cast<int64_t>(u) * per_unit;
+    const int64_t g_end = min(g + per_unit, total);
+    int b = 0;
+    int64_t base_b = 0;
+    if (g >= g_end || !locate_page(seq_lens, batch, bt_stride, hkv, g, b, base_b)) return;
+    int L = min(seq_lens[b], bt_stride * kPageSize);
+    int np_b = (L + kPageSize - 1) / kPageSize;
+    int kvh = static_cast<int>((g - base_b) / np_b);
+    int off = static_cast<int>((g - base_b) % np_b);
+    for (bool first = true; g < g_end; first = false) {
+        const int n = static_cast<int>(min(static_cast<int64_t>(np_b - off), g_end - g));
+        if (!first) __syncthreads();  // the previous piece's merge is done with the LDS
+        decode_pages(kpool, vpool, q, out, bt + static_cast<size_t>(b) * bt_stride, ws_o, ws_ml, b, L, hkv, kvh,
+                     group, num_pages, scale_log2, off, off + n, true, off == 0 && n == np_b,
+                     static_cast<int64_t>(u) + static_cast<int64_t>(b) * hkv + kvh, tid, s_v, s_m, s_l);
+        if (off == 0 && kvh == 0 && tid == 0) ws_cbase[b] = static_cast<int32_t>(base_b);
+        g += n;
+        off = 0;
+        if (++kvh == hkv) {
+            kvh = 0;
+            base_b += static_cast<int64_t>(hkv) * np_b;
+            if (++b >= batch) break;
+            L = min(seq_lens[b], bt_stride * kPageSize);
+            np_b = (L + kPageSize - 1) / kPageSize;
+            if (np_b == 0) break;  // device lengths that disagree with the host's
+        }
+    }
 }
 
 }  // namespace dk

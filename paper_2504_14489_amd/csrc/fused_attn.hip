@@ -77,7 +77,7 @@ extern "C" mw_status mw_fused_attn(const mw_prefill_args *pre, const mw_decode_a
     mw_status st = prefill_prepare(pre, stream_cus(s), false, &pp, who);  // 8-wave work-groups only
     if (st != MW_OK) return st;
     DecodePlan dp;
-    st = decode_prepare(dec, &dp, who);
+    st = decode_prepare(dec, 0, &dp, who);  // fixed chunks: a fused work-group's barriers are uniform
     if (st != MW_OK) return st;
     const int64_t n_pre = pp.gx * pp.batch, n_dec = (dp.units + 1) / 2;
     if (n_pre + n_dec > 0x7fffffff) return fail(MW_ERR_UNSUPPORTED, "%s: grid too large", who);

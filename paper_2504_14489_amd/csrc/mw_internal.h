@@ -76,14 +76,19 @@ namespace mw {
 // Checked launch parameters of one decode call (shared by mw_decode_attn and
 // the fused kernel's launcher).
 struct DecodePlan {
-    int64_t units;        // (chunk, kv head) work units of the split kernel
-    int chunk_pages;      // resolved chunk length (0 chooses from the lengths)
-    size_t off_ml, off_cbase, bytes;  // workspace layout: partial O, (m, l), chunk bases
+    int64_t units;        // work-groups of the split kernel
+    int chunk_pages;      // fixed chunks: resolved chunk length; 0 with the balanced split
+    int64_t per_unit;     // balanced split: pages per unit (0 with fixed chunks)
+    int64_t total;        // balanced split: pages of all (sequence, kv head) segments
+    int64_t slots;        // partial slots in the workspace
+    size_t off_ml, off_cbase, bytes;  // workspace layout: partial O, (m, l), per-sequence bases
     int hkv, group;
     float scale_log2;
 };
 // Validates a decode call's arguments (workspace size included) and plans it.
-mw_status decode_prepare(const mw_decode_args *a, DecodePlan *p, const char *who);
+// cus > 0 with chunk_pages = 0: the balanced split over that many CUs;
+// cus = 0: fixed chunks only (chunk_pages 0 then means automatic chunks).
+mw_status decode_prepare(const mw_decode_args *a, int64_t cus, DecodePlan *p, const char *who);
 // Launches the kernel that merges the chunk partials of every (sequence, kv head).
 mw_status decode_combine_launch(const mw_decode_args *a, const DecodePlan &p, hipStream_t s);
 

@@ -190,7 +190,7 @@ def main(argv=None):
     k.add_argument("--command", required=True)
     k.add_argument("--trace-last", type=int, default=0)
     k.add_argument("--skip-last", type=int, default=0)
-    k.add_argument("--kernels", default="k_prefill_attn,k_decode_split")
+    k.add_argument("--kernels", default="k_prefill_attn,k_decode_balanced")
     k.add_argument("--note", default="")
     k.add_argument("--out", required=True)
     m = sub.add_parser("mfma")

@@ -204,3 +204,16 @@ def test_engine_structs_match_the_header(tmp_path):
         cls = structs[cname]
         want = ctypes.sizeof(cls) if field == "size" else getattr(cls, field).offset
         assert int(val) == want, (cname, field, val, want)
+
+
+def test_decode_workspace_covers_both_splits():
+    """The workspace size for chunk_pages 0 fits the balanced split on any
+    stream and the fixed chunks that the fused call takes for 0."""
+    from paper_2504_14489_amd import mw, workloads as W
+    lens = W.make_workload(W.custom_config(hq=32, hkv=8, pre_chunks=((0, 1),), dec_batch=64,
+                                           dec_len_lo=1, dec_len_hi=4096, seed=3)).dec_lens
+    size0 = mw.mw_decode_workspace_size(32, 8, 128, lens, 0)
+    assert size0 >= mw.mw_decode_workspace_size(32, 8, 128, lens, -1)
+    # largest balanced split: 512 ranges, a piece of each (range, segment)
+    # boundary: (512 + 64 * 8 - 1) slots of 4 heads x 128 fp32 + (m, l)
+    assert size0 >= (512 + 64 * 8 - 1) * 4 * (128 * 4 + 8)

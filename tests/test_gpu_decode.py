@@ -37,7 +37,7 @@ def test_decode_matches_oracle_on_edge_lengths(hq, hkv, q_scale):
     assert_close(got, ref, f"decode hq={hq} hkv={hkv}")
 
 
-@pytest.mark.parametrize("chunk_pages", [8, 16, 32, 64])
+@pytest.mark.parametrize("chunk_pages", [8, 16, 32, 64, -1])
 def test_decode_split_count_invariance(chunk_pages):
     say(f"decode chunk_pages={chunk_pages}")
     cfg = W.custom_config(hq=32, hkv=8, pre_chunks=((0, 1),), dec_batch=12, dec_len_lo=1,
@@ -123,3 +123,45 @@ def test_decode_wide_score_range():
     got = run_decode(wl)
     ref = oracle.decode(wl.q_dec, wl.k_pool, wl.v_pool, wl.dec_bt, wl.dec_lens)
     assert_close(got, ref, "decode wide score range")
+
+
+# (name, hq, hkv, batch, shortest, longest): long sequences whose segments the
+# balanced ranges cut, and many 1..3-page sequences several of whose segments
+# fall in one range
+BALANCED_CASES = [("long", 32, 8, 24, 1, 3000), ("short", 8, 2, 300, 1, 40), ("group16", 16, 1, 5, 700, 4100)]
+
+
+@pytest.mark.parametrize("decode_cus", [8, 64, 192, 256])
+@pytest.mark.parametrize("case", BALANCED_CASES, ids=[c[0] for c in BALANCED_CASES])
+def test_decode_balanced_split_on_partitions(case, decode_cus):
+    """The balanced split (chunk_pages 0) cuts the pages into 2 ranges per CU
+    of the stream: every partition size gives the oracle's result, run to run
+    bit for bit, and the same bits as a second stream of that size."""
+    from paper_2504_14489_amd.device import Partition
+    name, hq, hkv, batch, lo, hi = case
+    say(f"decode balanced {name} on {decode_cus} CUs")
+    cfg = W.custom_config(hq=hq, hkv=hkv, pre_chunks=((0, 1),), dec_batch=batch, dec_len_lo=lo,
+                          dec_len_hi=hi, seed=50 + batch)
+    wl = W.make_workload(cfg)
+    dw = DeviceWorkload(wl)
+    parts = []
+    try:
+        if decode_cus < 256:
+            parts = [Partition(256 - decode_cus, decode_cus), Partition(256 - decode_cus, decode_cus)]
+            streams = [p.decode_stream for p in parts]
+        else:
+            streams = [0, torch.cuda.Stream().cuda_stream]
+        outs = []
+        for st in streams + streams[:1]:
+            o = dw.decode(st)
+            torch.cuda.synchronize()
+            outs.append(to_bits(o))
+    finally:
+        for p in parts:
+            p.close()
+        dw.close()
+    assert np.array_equal(outs[0], outs[2]), "run-to-run results differ"
+    assert np.array_equal(outs[0], outs[1]), "two streams of one size differ"
+    ref = oracle.decode(wl.q_dec, wl.k_pool, wl.v_pool, wl.dec_bt, wl.dec_lens)
+    assert_close(outs[0], ref, f"decode balanced {name} on {decode_cus} CUs")
+

@@ -25,12 +25,14 @@ CASES = {
 
 
 def separate(dw, dec, pre, stream):
+    # the fused call takes chunk_pages 0 as automatic fixed chunks (-1)
+    ch = dec.get("chunk_pages", 0) or -1
     mw.mw_prefill_attn(pre["pool"], dw.hq, dw.hkv, dw.d, dw.scale, pre["new_lens"], pre["prefix_lens"],
                        pre["d_qo_indptr"], pre["d_prefix_lens"], pre["d_block_table"], pre["bt_stride"],
                        pre["d_q"], pre["d_out"], stream, None)
     mw.mw_decode_attn(dec["pool"], dw.hq, dw.hkv, dw.d, dw.scale, dw.dec_lens, dec["d_seq_lens"],
                       dec["d_block_table"], dec["bt_stride"], dec["d_q"], dec["d_out"], dec["d_workspace"],
-                      dec["workspace_bytes"], dec.get("chunk_pages", 0), stream, None)
+                      dec["workspace_bytes"], ch, stream, None)
     mw.mw_sync(stream)
     return dw.o_pre.clone(), dw.o_dec.clone()
 
