@@ -240,7 +240,10 @@ def main(argv=None):
                     "device_bytes_seen_by_torch": free0 - torch.cuda.mem_get_info()[0]}
     log(f"[engine] group of {len(p_list)} partitions: {mem_bytes / 2**20:.2f} MiB, {create_ms:.2f} ms")
 
-    # reference outputs of one call each, on the whole device
+    # reference outputs of one call each, on the whole device (the decode
+    # reference is taken again on each partition's decode stream below: the
+    # balanced decode split depends on the stream's CU count, the prefill
+    # result does not)
     whole_p, whole_d = eng.streams(-1)
     mw.mw_decode_attn(dec["pool"], dw.hq, dw.hkv, dw.d, dw.scale, dw.dec_lens, dec["d_seq_lens"],
                       dec["d_block_table"], dec["bt_stride"], dec["d_q"], dec["d_out"], dec["d_workspace"],
@@ -268,6 +271,7 @@ def main(argv=None):
                                        pre["d_block_table"], pre["bt_stride"], pre["d_q"], pre["d_out"], ps, t.h)
                     mw.mw_sync(ps)
             t_d, t_p = td.elapsed()[0], tp.elapsed()[0]
+            ref_dec = dw.o_dec.clone()  # the solo decode calls ran on this partition's decode stream
             log(f"[engine] partition {p_cus}: decode layer {t_d:.3f} ms, prefill layer {t_p:.3f} ms")
             part = {"prefill_cus": p_cus, "decode_layer_ms": t_d, "prefill_layer_ms": t_p, "scenarios": {}}
             e_d, e_p = t_d, t_p

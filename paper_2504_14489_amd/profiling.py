@@ -146,11 +146,66 @@ def pair_slowdown(pre: PrefillCall, dec: DecodeCall, part: Partition, pre_ms: fl
 
 
 def work_groups(sample, phase) -> int:
-    """Work-groups of the call (query blocks of 64 positions x kv heads for
-    prefill, chunks of 32 pages x kv heads for decode)."""
+    """Work-groups of the call: query blocks of 64 positions x kv heads for
+    prefill; for decode the balanced split's page ranges (two per CU, at
+    least 8 pages each)."""
     if phase == 0:
         return (sample["n"] + 63) // 64 * HKV
-    return sum((L + 32 * PAGE - 1) // (32 * PAGE) for L in sample["lens"]) * HKV
+    pages = sum((L + PAGE - 1) // PAGE for L in sample["lens"]) * HKV
+    return min(2 * sample["cus"], (pages + 7) // 8)
+
+
+def write_table(result, path, command):
+    """The profiling summary as Markdown: grid, predictor accuracy per phase
+    and partition size, contention guard."""
+    g, m = result["grid"], result["model"]
+    pcus = sorted({s["cus"] for s in result["prefill"]})
+    dcus = sorted({s["cus"] for s in result["decode"]})
+    held = sum(1 for s in result["prefill"] if not s["grid"]) // max(len(pcus), 1)
+    lines = [f"# Estimator profiling: solo-run predictor and contention guard "
+             f"({m['num_q_heads']} q-heads / {m['num_kv_heads']} kv-heads attention shape)", "",
+             "Command (on the MI355X box):", "", f"    {command}", "",
+             f"Model shape: {m['num_q_heads']} query heads, {m['num_kv_heads']} kv heads, head_dim {m['head_dim']}, "
+             f"{m['page_size']}-token pages; random bf16 K/V and Q on the device.",
+             f"Grid (powers of 4, as the paper samples; scaled to one GPU): prefill new tokens {g['prefill_new']}, "
+             f"reused {g['prefill_reused']}; decode batch {g['decode_batch']} with every sequence of length "
+             f"{g['decode_len']}; prefill/decode CUs " + ", ".join(f"{p}/{256 - p}" for p in pcus) + ".  "
+             f"Held-out samples: {held} random prefill (n, r) and {held} random decode batches (random lengths per "
+             "sequence) per partition.  Solo = median of the calls alone on the partition's CUs; decode = whole "
+             "call (split + combine kernels, balanced split).", "",
+             "## Solo-run predictor (Eqs. (1)-(2), least squares of the relative error)", "",
+             "| phase | CUs | theta (ms per unit) | max deviation, grid (train) | max deviation, held out |",
+             "|---|---|---|---|---|"]
+    for phase, cus_list in (("prefill", pcus), ("decode", dcus)):
+        nth = 4 if phase == "prefill" else 3
+        for c in cus_list:
+            e = result["predictor"][phase][str(c)] if str(c) in result["predictor"][phase] \
+                else result["predictor"][phase][c]
+            th = ", ".join(f"{x:.3g}" for x in e["theta"][:nth])
+            lines.append(f"| {phase} | {c} | {th} | {100 * e['max_dev']['train']:.1f}% | "
+                         f"{100 * e['max_dev']['held_out']:.1f}% |")
+    lines += ["", "For comparison, the paper's predictor misses whole-model iterations on NVIDIA GPUs by at most "
+              "8.16% (prefill) and 8.84% (decode).  Single attention calls keep the step changes of a launch "
+              "(rounds of work-groups over the partition's CUs, paired or single query blocks), which "
+              "linear-in-work models miss, most on 192 CUs."]
+    gd = result["guard"]
+    sl = sorted(s["slowdown"] for s in result["pairs"] if s["slowdown"] is not None)
+    p90 = sl[int(0.9 * (len(sl) - 1))] if sl else float("nan")
+    lines += ["", "## Contention guard (decode slowdown = multiplexed / solo call latency on the same CUs)", "",
+              f"{gd['pairs']} pairs, {gd['pairs_measured']} measured; slowdown median "
+              f"{gd['median_slowdown']:.3f}, 90th percentile {p90:.3f}, maximum {gd['max_slowdown']:.3f} "
+              "(the paper measures up to 20% on A100 and 30% on H100).", "",
+              "| prefill CUs | max decode slowdown | at (prefill new, reused, decode batch, decode reused tokens) |",
+              "|---|---|---|"]
+    for c in pcus:
+        ps = [s for s in result["pairs"] if s["prefill_cus"] == c and s["slowdown"] is not None]
+        if ps:
+            w = max(ps, key=lambda s: s["slowdown"])
+            lines.append(f"| {c} | {w['slowdown']:.3f} | ({w['prefill_new']}, {w['prefill_reused']}, "
+                         f"{w['decode_batch']}, {w['decode_reused']}) |")
+    lines += ["", f"Whole sweep: {result['seconds']:.0f} s of wall time.", ""]
+    with open(path, "w") as f:
+        f.write("\n".join(lines))
 
 
 def fit_and_score(samples, train_filter, phase):
@@ -199,6 +254,7 @@ def main(argv=None):
     ap.add_argument("--held-out", type=int, default=10, help="random held-out samples per partition and phase")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--quick", action="store_true", help="a small grid (functional check)")
+    ap.add_argument("--table", default="", help="also write the Markdown summary here")
     args = ap.parse_args(argv)
     torch.cuda.init()
     grid_n = [1024, 4096, 16384]
@@ -283,6 +339,9 @@ def main(argv=None):
         ", ".join(f"{c} CUs {100 * v['max_dev']['held_out']:.1f}%" for c, v in pr["prefill"].items()) +
         "; decode " + ", ".join(f"{c} CUs {100 * v['max_dev']['held_out']:.1f}%" for c, v in pr["decode"].items()))
     log(f"[profiling] guard: max slowdown {result['guard']['max_slowdown']}, {result['seconds']:.0f}s total")
+    if args.table:
+        write_table(result, args.table, "python3 -m paper_2504_14489_amd.profiling " + " ".join(
+            argv if argv is not None else sys.argv[1:]))
 
 
 if __name__ == "__main__":

@@ -28,9 +28,11 @@ def setup():
     dw.close()
 
 
-def _plain_outputs(dw, eng, dec, pre):
-    """One decode and one prefill call on the whole device."""
-    ps, ds = eng.streams(-1)
+def _plain_outputs(dw, eng, dec, pre, config=-1):
+    """One decode and one prefill call on the streams of partition `config`
+    (-1: the whole device).  The decode split depends on the stream's CU
+    count, so a run on a partition is compared with a call on its stream."""
+    ps, ds = eng.streams(config)
     mw.mw_decode_attn(dec["pool"], dw.hq, dw.hkv, dw.d, dw.scale, dw.dec_lens, dec["d_seq_lens"],
                       dec["d_block_table"], dec["bt_stride"], dec["d_q"], dec["d_out"], dec["d_workspace"],
                       dec["workspace_bytes"], 0, ds, None)
@@ -65,7 +67,7 @@ def test_engine_batch_of_chunks_matches_oracle(setup):
 def test_engine_runs_leave_outputs_unchanged(setup, policy, npl, switch, config):
     wl, dw, eng, dec, pre = setup
     say(f"engine run: policy {policy} N_PL {npl} switch {switch} partition {config}")
-    ref_dec, ref_pre = _plain_outputs(dw, eng, dec, pre)
+    ref_dec, ref_pre = _plain_outputs(dw, eng, dec, pre, config)
     dw.o_dec.zero_()
     dw.o_pre.zero_()
     torch.cuda.synchronize()
@@ -137,7 +139,7 @@ def test_engine_decode_graph_replays_match_eager(setup):
     serves every run with the same arguments and partition."""
     wl, dw, eng, dec, pre = setup
     say("engine decode graph replays")
-    ref_dec, ref_pre = _plain_outputs(dw, eng, dec, pre)
+    ref_dec, ref_pre = _plain_outputs(dw, eng, dec, pre, 0)
     n0 = eng.graphs()[0]
     for rep in range(4):
         dw.o_dec.zero_()
@@ -150,7 +152,7 @@ def test_engine_decode_graph_replays_match_eager(setup):
         assert torch.equal(dw.o_pre, ref_pre), f"replay {rep}"
         assert mw.mw_engine_timeline(eng.h, 0).shape == (3, 3)      # one span per iteration
         assert s["decode_iter_ms_mean"] > 0.0
-        _plain_outputs(dw, eng, dec, pre)                            # eager work between replays
+        _plain_outputs(dw, eng, dec, pre, 0)                         # eager work between replays
     n1, nbytes, ms = eng.graphs()
     assert n1 == n0 + 1 and nbytes >= 0 and ms > 0.0
     eng.run(dec, pre, config=1, decode_iters=1, decode_layers=4, prefill_layers=2, layers_per_launch=1,
