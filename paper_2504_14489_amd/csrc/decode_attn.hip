@@ -40,8 +40,8 @@ k_decode_balanced(const uint16_t *__restrict__ kpool, const uint16_t *__restrict
                 scale_log2, per_unit, total, blockIdx.x, threadIdx.x, s_v, s_m, s_l);
 }
 
-// One work-group per (sequence, kv head); thread pairs (h, d).  The partials
-// of the segment's pieces are loaded with independent loads (8 in flight).
+// One work-group per (sequence, kv head), each thread merging two outputs
+// (h, d) of the segment's pieces.
 // Fixed chunks (per_unit = 0): chunk c of sequence b is slot
 // (ws_cbase[b] + c) hkv + kv head.  Balanced split (per_unit > 0): the
 // segment starts at global page P = ws_cbase[b] + kv head * pages(b), and its
@@ -72,39 +72,44 @@ k_decode_combine(uint16_t *__restrict__ out, const int32_t *__restrict__ seq_len
     // outside the workspace
     if (first < 0 || first + static_cast<int64_t>(nch - 1) * stride >= slots) return;
     const int hq = hkv * group;
-    for (int idx = threadIdx.x; idx < group * kHeadDim; idx += kThreads) {
-        const int h = idx / kHeadDim, d = idx % kHeadDim;
-        float M = -INFINITY;
+    // One pass over the pieces with a running maximum; each thread merges two
+    // outputs (h, d), and the (m, l) and o of 8 pieces of both are loaded
+    // together, so a short segment costs one round of loads.
+    const int n_out = group * kHeadDim;
+    for (int i0 = threadIdx.x; i0 < n_out; i0 += 2 * kThreads) {
+        const int idx[2] = {i0, i0 + kThreads};
+        float M[2] = {-INFINITY, -INFINITY}, lsum[2] = {0.f, 0.f}, osum[2] = {0.f, 0.f};
         for (int s0 = 0; s0 < nch; s0 += 8) {
-            float2 ml[8];
+            float2 ml[2][8];
+            float o[2][8];
 #pragma unroll
-            for (int j = 0; j < 8; ++j)
-                ml[j] = s0 + j < nch ? ws_ml[static_cast<size_t>(first + (s0 + j) * stride) * group + h]
-                                     : make_float2(-INFINITY, 0.f);
+            for (int k = 0; k < 2; ++k)
 #pragma unroll
-            for (int j = 0; j < 8; ++j)
-                if (ml[j].y > 0.f) M = fmaxf(M, ml[j].x);
+                for (int j = 0; j < 8; ++j) {
+                    const bool in = s0 + j < nch && idx[k] < n_out;
+                    const int h = in ? idx[k] / kHeadDim : 0, d = idx[k] % kHeadDim;
+                    const size_t uu = static_cast<size_t>(first + (s0 + j) * stride) * group + h;
+                    ml[k][j] = in ? ws_ml[uu] : make_float2(-INFINITY, 0.f);
+                    o[k][j] = in ? ws_o[uu * kHeadDim + d] : 0.f;
+                }
+#pragma unroll
+            for (int k = 0; k < 2; ++k)
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    if (!(ml[k][j].y > 0.f)) continue;  // a piece without keys contributes nothing
+                    const float mn = fmaxf(M[k], ml[k][j].x);
+                    const float a = __builtin_amdgcn_exp2f(M[k] - mn), w = __builtin_amdgcn_exp2f(ml[k][j].x - mn);
+                    lsum[k] = lsum[k] * a + w * ml[k][j].y;
+                    osum[k] = osum[k] * a + w * o[k][j];
+                    M[k] = mn;
+                }
         }
-        float lsum = 0.f, osum = 0.f;
-        for (int s0 = 0; s0 < nch; s0 += 8) {
-            float2 ml[8];
-            float o[8];
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const size_t uu = static_cast<size_t>(first + (s0 + j) * stride) * group + h;
-                const bool in = s0 + j < nch;
-                ml[j] = in ? ws_ml[uu] : make_float2(-INFINITY, 0.f);
-                o[j] = in ? ws_o[uu * kHeadDim + d] : 0.f;
+        for (int k = 0; k < 2; ++k)
+            if (idx[k] < n_out) {
+                const int h = idx[k] / kHeadDim, d = idx[k] % kHeadDim;
+                out[(static_cast<size_t>(b) * hq + kvh * group + h) * kHeadDim + d] = to_bf16(osum[k] / lsum[k]);
             }
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                if (!(ml[j].y > 0.f)) continue;  // a chunk without keys contributes nothing
-                const float w = __builtin_amdgcn_exp2f(ml[j].x - M);
-                lsum += w * ml[j].y;
-                osum += w * o[j];
-            }
-        }
-        out[(static_cast<size_t>(b) * hq + kvh * group + h) * kHeadDim + d] = to_bf16(osum / lsum);
     }
 }
 
