@@ -96,7 +96,7 @@ def test_decode_workspace_size(lib):
         with pytest.raises(mw.MWError) as e:
             mw.mw_decode_workspace_size(*args)
         assert e.value.status == status
-    for bad in (4, 12, 264):
+    for bad in (4, 12, 264, -2, -8):
         with pytest.raises(mw.MWError) as e:
             mw.mw_decode_workspace_size(8, 2, 128, [5], bad)
         assert e.value.status == mw.MW_ERR_UNSUPPORTED
