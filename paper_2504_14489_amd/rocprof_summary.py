@@ -77,12 +77,12 @@ def traffic(args):
     f_scale, w_scale = kib / f_copy, kib / w_copy
     lines = [f"# HBM traffic per launch: {args.workload} workload", "",
              "Commands (on the MI355X box, from /tmp with TMPDIR=/tmp; one counter per run):", "",
-             f"    rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_FETCH_SIZE -o run -- "
+             f"    rocprofv3 --pmc FETCH_SIZE --output-format csv -d {args.fetch} -o run -- "
              f"python3 bench.py --config {args.workload} --traffic-pass",
-             f"    rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_WRITE_SIZE -o run -- "
+             f"    rocprofv3 --pmc WRITE_SIZE --output-format csv -d {args.write} -o run -- "
              f"python3 bench.py --config {args.workload} --traffic-pass",
              f"    python -m paper_2504_14489_amd.rocprof_summary traffic --workload {args.workload} "
-             f"--fetch gpurun_out/pmc_FETCH_SIZE --write gpurun_out/pmc_WRITE_SIZE --out <this file>", "",
+             f"--fetch {args.fetch} --write {args.write} --out <this file>", "",
              "bench.py --traffic-pass runs one isolated launch of each kernel on its partition and a "
              f"device-to-device copy of {COPY_BYTES} bytes ({COPY_KERNEL}) that calibrates the counters.", "",
              f"# copy calibration: FETCH_SIZE read {f_copy:.1f} KiB and WRITE_SIZE {w_copy:.1f} KiB for "
@@ -124,9 +124,9 @@ def mfma(args):
     lines = [f"# Matrix-core use of k_prefill_attn: {args.workload} workload, first prefill chunk on {args.cus} CUs",
              "", "Commands (on the MI355X box, from /tmp with TMPDIR=/tmp):", "",
              f"    rocprofv3 --pmc SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE "
-             f"--output-format csv -d gpurun_out/pmc_mfma -o run -- python3 bench.py --config {args.workload} "
+             f"--output-format csv -d {args.dir} -o run -- python3 bench.py --config {args.workload} "
              f"--traffic-pass",
-             f"    python -m paper_2504_14489_amd.rocprof_summary mfma --dir gpurun_out/pmc_mfma --workload "
+             f"    python -m paper_2504_14489_amd.rocprof_summary mfma --dir {args.dir} --workload "
              f"{args.workload} --cus {args.cus} --out <this file>", "",
              f"k_prefill_attn.mfma_bf16_flop: {mops * 512:.0f}",
              f"k_prefill_attn.algorithmic_flop: {algo:.0f}",
