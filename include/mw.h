@@ -166,9 +166,10 @@ mw_status mw_partition_destroy(mw_partition *part);
  * hardware ids of the CU they run on and a start/end timestamp:
  * d_out[4*b + 0] = XCC id, [+1] = HW_ID register (CU, SIMD, shader array,
  * shader engine fields), [+2] = start and [+3] = end of a spin of spin_cycles
- * shader clocks (low 32 bits of the 100 MHz real-time counter). */
+ * shader clocks (low 32 bits of the 100 MHz real-time counter).  `timing`
+ * may be NULL; given one, it records the launch as one kernel. */
 mw_status mw_cu_probe(int32_t n_blocks, int32_t spin_cycles, uint32_t *d_out,
-                      mw_stream stream);
+                      mw_stream stream, mw_timing *timing);
 
 /* Measured HBM read ceiling: reads `bytes` (a multiple of 16, 16-byte aligned)
  * from d_src once with n_blocks 256-thread work-groups on `stream` (so on that

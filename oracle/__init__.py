@@ -80,7 +80,18 @@ def _ptr(a: np.ndarray):
 
 
 def default_threads() -> int:
-    return max(1, min(os.cpu_count() or 1, 64))
+    """Host threads the oracle uses by default: the CPUs this process may run
+    on, capped by OMP_NUM_THREADS when that is set (a machine's share of its
+    cores for one job) and by 64."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        n = os.cpu_count() or 1
+    try:
+        n = min(n, int(os.environ.get("OMP_NUM_THREADS", n)))
+    except ValueError:
+        pass
+    return max(1, min(n, 64))
 
 
 def paged_attention(q: np.ndarray, k_pool: np.ndarray, v_pool: np.ndarray,

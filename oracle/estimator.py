@@ -47,12 +47,6 @@ def fit_relative(features: np.ndarray, times: np.ndarray) -> np.ndarray:
     return theta
 
 
-def max_relative_deviation(features: np.ndarray, times: np.ndarray, theta: np.ndarray) -> float:
-    pred = np.asarray(features, dtype=np.float64) @ theta
-    t = np.asarray(times, dtype=np.float64)
-    return float(np.max(np.abs(pred - t) / t))
-
-
 def cell(x: int, base: int) -> int:
     """Smallest k with base^k >= x (0 for x <= 1)."""
     k, v = 0, 1

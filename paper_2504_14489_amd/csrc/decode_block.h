@@ -178,13 +178,16 @@ decode_pages(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vp
         bool ok[kPair];
 #pragma unroll
         for (int j = 0; j < kPair; ++j) ok[j] = pr.ok[j];
-        // V of this pair -> LDS (as loaded; an absent page as zeros), then
-        // K -> S^T on the matrix core (scores of an absent page are masked)
+        // V of this pair -> LDS as loaded, with rows of an absent page or past
+        // the sequence's end as zeros (a masked key has p = 0, but 0 times a
+        // NaN or Inf in a slack slot would not be 0); then K -> S^T on the
+        // matrix core (scores of those keys are masked below)
 #pragma unroll
         for (int j = 0; j < kPair; ++j)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                *reinterpret_cast<uint4 *>(vbuf + (16 * j + 4 * i + grp) * VSTR + 8 * col) = sel4(pr.ok[j], pr.v[j][i]);
+                *reinterpret_cast<uint4 *>(vbuf + (16 * j + 4 * i + grp) * VSTR + 8 * col) =
+                    sel4(pr.ok[j] && (p0 + j) * kPageSize + 4 * i + grp < L, pr.v[j][i]);
         f32x4 sc[kPair];
 #pragma unroll
         for (int j = 0; j < kPair; ++j) {

@@ -170,8 +170,7 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
         const int np_wg = min(4 * nt_a, np_seq);
         for (int i = threadIdx.x; i < min(np_wg, kBtCache); i += kNT) s_bt[i] = btrow[i];
     }
-    const int first_page = btrow[0];
-    const int safe_page = (first_page >= 0 && first_page < num_pages) ? first_page : 0;
+    const int seq_len = r + n;
 
     // ---- per-lane byte offsets, computed once
     // K operand: row l32 (+32 rows for the second key block), logical chunk
@@ -210,32 +209,46 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
     float m_run = -INFINITY;
     float l_run = 0.f;
 
-    // Pool element offset of page `lpage` of key tile `it` (uniform).
-    auto page_base = [&](int page) __attribute__((always_inline)) {
-        // a page outside the pool is never read; a page past the sequence is
-        // read from the sequence's first page: those keys lie past every valid
-        // query and the causal mask discards them, and that page holds finite data
-        if (page < 0 || page >= num_pages) page = safe_page;
-        return (static_cast<size_t>(page) * hkv + kvh) * (kPageSize * kHeadDim);
+    // The (page, kv head) block of sequence page p (uniform per wave): its pool
+    // element offset and the bytes of it that hold the sequence's tokens.  A
+    // page past the sequence or outside the pool has 0 bytes, and the last page
+    // only its rows below r + n: the buffer loads return zeros past that, so
+    // slack slots and absent pages are never read, whatever bits they hold
+    // (zero keys and values past the sequence are also discarded by the causal
+    // mask: they lie after every query).
+    struct PageRef {
+        size_t base;
+        int bytes;
     };
-    auto table_entry = [&](int it) __attribute__((always_inline)) {
+    auto page_ref = [&](int p, int page) __attribute__((always_inline)) {
+        const bool ok = p < np_seq && page >= 0 && page < num_pages;
+        PageRef ref;
+        ref.base = ok ? (static_cast<size_t>(page) * hkv + kvh) * (kPageSize * kHeadDim) : 0;
+        ref.bytes = ok ? min(seq_len - kPageSize * p, kPageSize) * (kHeadDim * 2) : 0;
+        return ref;
+    };
+    // Page `lpage` of key tile `it`, its entry read from the LDS copy of the table.
+    auto tile_page = [&](int it) __attribute__((always_inline)) {
         const int p = 4 * it + lpage;
-        if (p >= np_seq) return -1;
-        if constexpr (kTableInLds)
-            return __builtin_amdgcn_readfirstlane(s_bt[p]);
-        else
-            return p < kBtCache ? __builtin_amdgcn_readfirstlane(s_bt[p]) : btrow[p];
+        int page = -1;
+        if (p < np_seq) {
+            if constexpr (kTableInLds)
+                page = __builtin_amdgcn_readfirstlane(s_bt[p]);
+            else
+                page = p < kBtCache ? __builtin_amdgcn_readfirstlane(s_bt[p]) : btrow[p];
+        }
+        return page_ref(p, page);
     };
     // Loads (1 KB each) of this wave's half page of one tile: buffer loads over
-    // a descriptor of the page (4 KB; the hardware returns zeros past it).
-    // Buffer rather than global loads: the compiler counts a global load into
-    // LDS as an outstanding LDS access too, which would make every operand read
-    // wait for all LDS reads in flight.  The LDS destination goes through an
-    // integer, so the compiler does not tie later LDS reads to these loads; the
-    // loop waits for them explicitly.
-    auto page_rsrc = [&](const uint16_t *pool, size_t base) __attribute__((always_inline)) {
-        return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(pool + base), 0,
-                                                 kPageSize * kHeadDim * 2, kBufferFormat);
+    // a descriptor of the page's valid rows (the hardware returns zeros past
+    // them).  Buffer rather than global loads: the compiler counts a global
+    // load into LDS as an outstanding LDS access too, which would make every
+    // operand read wait for all LDS reads in flight.  The LDS destination goes
+    // through an integer, so the compiler does not tie later LDS reads to these
+    // loads; the loop waits for them explicitly.
+    auto page_rsrc = [&](const uint16_t *pool, PageRef ref) __attribute__((always_inline)) {
+        return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(pool + ref.base), 0, ref.bytes,
+                                                 kBufferFormat);
     };
     auto page_load = [&](__amdgpu_buffer_rsrc_t rsrc, uint16_t *dst, int j) __attribute__((always_inline)) {
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
@@ -349,9 +362,8 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
     // The first tile of an item: its pages straight from the block table in
     // HBM, so the loads can start before the table copy in LDS is complete.
     auto first_tile = [&]() __attribute__((always_inline)) {
-        const int p = lpage;
-        const size_t base = page_base(p < np_seq ? btrow[p] : -1);
-        const __amdgpu_buffer_rsrc_t rk = page_rsrc(kpool, base), rv = page_rsrc(vpool, base);
+        const PageRef ref = page_ref(lpage, lpage < np_seq ? btrow[lpage] : -1);
+        const __amdgpu_buffer_rsrc_t rk = page_rsrc(kpool, ref), rv = page_rsrc(vpool, ref);
 #pragma unroll
         for (int j = 0; j < kJ; ++j) {
             page_load(rk, s_k, j);
@@ -389,8 +401,8 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
         // the K and V pages of a tile are the same pages of the pool.
         for (int t = 0; t < nt; ++t) {
             const bool more = t + 1 < nt;
-            const size_t base = page_base(more ? table_entry(t + 1) : 0);
-            const __amdgpu_buffer_rsrc_t rk = page_rsrc(kpool, base), rv = page_rsrc(vpool, base);
+            const PageRef ref = more ? tile_page(t + 1) : PageRef{0, 0};
+            const __amdgpu_buffer_rsrc_t rk = page_rsrc(kpool, ref), rv = page_rsrc(vpool, ref);
             uint16_t *dk = s_k + ((t + 1) & 1) * TILE;
             uint16_t *dv = s_v + ((t + 1) & 1) * TILE;
             auto load = [&](int j) __attribute__((always_inline)) {

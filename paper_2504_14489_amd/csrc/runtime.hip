@@ -80,7 +80,7 @@ extern "C" {
 
 const char *mw_last_error(void) { return g_last_error; }
 
-int32_t mw_version(void) { return 1; }
+int32_t mw_version(void) { return 2; }
 
 mw_status mw_sync(mw_stream stream) {
     MW_HIP_TRY(hipStreamSynchronize(static_cast<hipStream_t>(stream)));
@@ -284,12 +284,18 @@ __global__ void __launch_bounds__(64) k_cu_probe(uint32_t *out, int spin_cycles)
 }
 
 extern "C" mw_status mw_cu_probe(int32_t n_blocks, int32_t spin_cycles, uint32_t *d_out,
-                                 mw_stream stream) {
+                                 mw_stream stream, mw_timing *timing) {
     if (n_blocks < 1 || n_blocks > (1 << 20) || spin_cycles < 0 || spin_cycles > (1 << 26) || !d_out)
         return fail(MW_ERR_INVALID_ARG, "mw_cu_probe: bad arguments");
-    hipLaunchKernelGGL(k_cu_probe, dim3(n_blocks), dim3(64), 0, static_cast<hipStream_t>(stream),
-                       d_out, spin_cycles);
-    return check_launch("k_cu_probe");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    mw_status st = timing_begin(timing, s);
+    if (st != MW_OK) return st;
+    hipLaunchKernelGGL(k_cu_probe, dim3(n_blocks), dim3(64), 0, s, d_out, spin_cycles);
+    st = check_launch("k_cu_probe");
+    if (st != MW_OK) return st;
+    st = timing_kernel_done(timing, s);
+    timing_end(timing);
+    return st;
 }
 
 // ------------------------------------------------------- stream read ------

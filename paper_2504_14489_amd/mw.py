@@ -115,7 +115,7 @@ _SIGNATURES = {
     "mw_partition_streams": ([_P, ctypes.POINTER(_P), ctypes.POINTER(_P)], _I),
     "mw_partition_masks": ([_P, _PU, _PU], _I),
     "mw_partition_destroy": ([_P], _I),
-    "mw_cu_probe": ([_I, _I, _P, _P], _I),
+    "mw_cu_probe": ([_I, _I, _P, _P, _P], _I),
     "mw_stream_read": ([_P, ctypes.c_size_t, _P, _I, _P, _P], _I),
     "mw_timing_create": ([ctypes.POINTER(_P)], _I),
     "mw_timing_destroy": ([_P], _I),
@@ -296,8 +296,8 @@ def mw_partition_destroy(part):
     _check(load().mw_partition_destroy(part))
 
 
-def mw_cu_probe(n_blocks: int, spin_cycles: int, d_out: int, stream=0):
-    _check(load().mw_cu_probe(n_blocks, spin_cycles, _h(d_out), _h(stream)))
+def mw_cu_probe(n_blocks: int, spin_cycles: int, d_out: int, stream=0, timing=None):
+    _check(load().mw_cu_probe(n_blocks, spin_cycles, _h(d_out), _h(stream), timing))
 
 
 def mw_stream_read(d_src: int, nbytes: int, d_sink: int, n_blocks: int, stream=0, timing=None):

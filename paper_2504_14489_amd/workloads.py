@@ -45,6 +45,8 @@ import numpy as np
 PAGE_SIZE = 16
 HEAD_DIM = 128
 BF16_NAN = 0x7FC0
+BF16_POS_INF = 0x7F80
+BF16_NEG_INF = 0xFF80
 # 29952.0 in bf16 (0x46EA): finite, and large enough that an unmasked slack key
 # would dominate every softmax row it leaks into.
 BF16_SLACK_POISON = 0x46EA
@@ -232,12 +234,16 @@ def _normal_bf16(rng: np.random.Generator, shape, scale: float = 1.0) -> np.ndar
 
 
 def make_workload(cfg: Config, seed: Optional[int] = None, q_scale: float = 1.0,
-                  dec_lens: Optional[np.ndarray] = None) -> Workload:
+                  dec_lens: Optional[np.ndarray] = None,
+                  slack_bits: Tuple[int, int] = (BF16_SLACK_POISON, BF16_SLACK_POISON)) -> Workload:
     """Build the pool image, block tables and queries for ``cfg``.
 
     ``q_scale`` multiplies Q before rounding (a "peaked" variant that makes
     the running softmax maximum move).  ``dec_lens`` overrides the drawn decode
     lengths (the draw still happens, keeping the stream order fixed).
+    ``slack_bits`` are the bf16 patterns written to the K and V slots past each
+    sequence's end in its last page (default: the large finite poison; tests
+    also use NaN and Inf there, which no correct kernel lets into a result).
     """
     seed = cfg.seed if seed is None else seed
     rng = np.random.Generator(np.random.PCG64(seed))
@@ -287,8 +293,8 @@ def make_workload(cfg: Config, seed: Optional[int] = None, q_scale: float = 1.0,
     def poison_tail(bt_row, length):
         if length % S:
             last = bt_row[length // S]
-            k_pool[last, :, length % S:, :] = BF16_SLACK_POISON
-            v_pool[last, :, length % S:, :] = BF16_SLACK_POISON
+            k_pool[last, :, length % S:, :] = slack_bits[0]
+            v_pool[last, :, length % S:, :] = slack_bits[1]
     if pre_len:
         poison_tail(pre_bt, pre_len)
     for b, L in enumerate(lens):

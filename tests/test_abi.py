@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported_and_bound(lib):
 
 
 def test_version_and_empty_error(lib):
-    assert mw.mw_version() == 1
+    assert mw.mw_version() == 2
 
 
 FAKE_K, FAKE_V = 0x10000, 0x20000     # aligned addresses that are never dereferenced

@@ -165,3 +165,18 @@ def test_decode_balanced_split_on_partitions(case, decode_cus):
     ref = oracle.decode(wl.q_dec, wl.k_pool, wl.v_pool, wl.dec_bt, wl.dec_lens)
     assert_close(outs[0], ref, f"decode balanced {name} on {decode_cus} CUs")
 
+
+
+@pytest.mark.parametrize("slack", [(W.BF16_NAN, W.BF16_NAN), (W.BF16_POS_INF, W.BF16_NEG_INF)],
+                         ids=["nan-nan", "inf-neginf"])
+@pytest.mark.parametrize("chunk_pages", [0, 8])
+def test_decode_ignores_nan_and_inf_in_slack_slots(slack, chunk_pages):
+    """Slots past each sequence's end in its last page hold NaN or Inf: the
+    keys there are masked and their values must never reach the output (the
+    balanced split and fixed chunks; lengths on and around page edges)."""
+    say(f"decode slack {slack} chunk_pages={chunk_pages}")
+    cfg = W.custom_config(hq=32, hkv=8, pre_chunks=((0, 1),), dec_batch=len(EDGE_LENS), seed=5)
+    wl = W.make_workload(cfg, dec_lens=EDGE_LENS, slack_bits=slack)
+    got = run_decode(wl, chunk_pages)
+    ref = oracle.decode(wl.q_dec, wl.k_pool, wl.v_pool, wl.dec_bt, wl.dec_lens)
+    assert_close(got, ref, f"decode slack chunk_pages={chunk_pages}")

@@ -210,3 +210,66 @@ def test_empty_batches_and_zero_length_sequences():
         assert_close(to_bits(out[:40]), ref, "zero-length neighbour")
     finally:
         dw.close()
+
+
+SLACKS = [(W.BF16_NAN, W.BF16_NAN), (W.BF16_POS_INF, W.BF16_NEG_INF), (W.BF16_NAN, W.BF16_POS_INF)]
+
+
+@pytest.mark.parametrize("slack", SLACKS, ids=["nan-nan", "inf-neginf", "nan-inf"])
+def test_prefill_ignores_nan_and_inf_in_slack_slots(slack):
+    """Slots past a sequence's end in its last page may hold any bits: a key
+    there is masked (p = 0), and its value must never be read, since 0 * NaN
+    and 0 * Inf are NaN.  Ragged lengths on the whole GPU (4-wave blocks) and
+    on 8 CUs (8-wave paired blocks for the largest case)."""
+    from paper_2504_14489_amd.device import Partition
+    cases = [((0, 1), 8, 2), ((5, 100), 8, 2), ((33, 17), 32, 8), ((100, 130), 16, 1), ((0, 509), 32, 8)]
+    part = Partition(8, 8)
+    try:
+        for (r, n), hq, hkv in cases:
+            say(f"prefill slack {slack} hq={hq} hkv={hkv} r={r} n={n}")
+            cfg = W.custom_config(hq=hq, hkv=hkv, pre_chunks=((r, n),), dec_batch=1, dec_len_lo=1,
+                                  dec_len_hi=2, seed=r + 3 * n)
+            wl = W.make_workload(cfg, slack_bits=slack)
+            assert (r + n) % 16, "the case must leave slack in its last page"
+            ref = oracle.prefill(wl.q_pre[r:r + n], wl.k_pool, wl.v_pool, wl.pre_bt, r)
+            dw = DeviceWorkload(wl)
+            try:
+                for stream in (0, part.prefill_stream):
+                    o = dw.prefill(r, n, stream)
+                    torch.cuda.synchronize()
+                    assert_close(to_bits(o), ref, f"prefill slack r={r} n={n} stream={'all' if stream == 0 else 8}")
+            finally:
+                dw.close()
+    finally:
+        part.close()
+
+
+def test_prefill_block_table_longer_than_the_lds_copy():
+    """A sequence of more than 4096 pages (65,536 tokens): the work-group's
+    copy of its block table in LDS holds the first 4096 entries and the rest
+    are read from global memory.  130 new tokens over a 70,001-token prefix
+    with one kv head: 4-wave blocks on the whole GPU, 8-wave paired blocks on
+    8 CUs; every row against the oracle."""
+    from paper_2504_14489_amd.device import Partition
+    r, n = 70001, 130
+    say(f"prefill long block table r={r} n={n}")
+    cfg = W.custom_config(hq=16, hkv=1, pre_chunks=((r, n),), dec_batch=1, dec_len_lo=1, dec_len_hi=2,
+                          seed=70)
+    wl = W.make_workload(cfg)
+    assert len(wl.pre_bt) > 4096
+    dw = DeviceWorkload(wl)
+    part = Partition(8, 8)
+    outs = []
+    try:
+        for stream in (0, part.prefill_stream):
+            o = dw.prefill(r, n, stream)
+            torch.cuda.synchronize()
+            outs.append(to_bits(o).copy())
+    finally:
+        part.close()
+        dw.close()
+    ref = oracle.prefill(wl.q_pre[r:r + n], wl.k_pool, wl.v_pool, wl.pre_bt, r)
+    for o, where in zip(outs, ("whole GPU", "8 CUs")):
+        mx, mean = assert_close(o, ref, f"long table on {where}")
+        say(f"  {where}: max-abs {mx:.3g} mean-abs {mean:.3g}")
+    assert np.array_equal(outs[0], outs[1]), "4-wave and 8-wave launches differ"
