@@ -262,6 +262,24 @@ mw_status mw_decode_attn(const mw_kv_pool *pool, const mw_attn_shape *shape, int
                          void *d_out, void *d_workspace, size_t workspace_bytes,
                          int32_t chunk_pages, mw_stream stream, mw_timing *timing);
 
+/* Decode attention that allocates nothing, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): mw_decode_attn with the same arguments, checks and
+ * results (the same kernels and split), except that its workspace is a
+ * library-owned static device array of 16 MiB per device, held until the
+ * process ends, instead of d_workspace.  The call makes no hipMalloc, hipFree
+ * or other allocating call; its first call on a device looks up that device's
+ * array.  A call whose split needs more than 16 MiB of workspace (see
+ * mw_decode_workspace_size) fails with MW_ERR_UNSUPPORTED before launching
+ * anything.  Nothing in the array needs clearing between calls: a call reads
+ * only what it wrote.  Every call on a device shares its array, so calls
+ * that may overlap in time on one device (two streams, two threads) race:
+ * order them on one stream or use mw_decode_attn.  No timing handle. */
+mw_status mw_decode_attn_noalloc(const mw_kv_pool *pool, const mw_attn_shape *shape, int32_t batch,
+                                 const int32_t *h_seq_lens, const int32_t *d_seq_lens,
+                                 const int32_t *d_block_table, int32_t bt_stride, const void *d_q,
+                                 void *d_out, int32_t chunk_pages, mw_stream stream);
+
 /* ------------------------------------------------------------------------ *
  * Contention-tolerant estimator (paper Sec. 3.3) and the prefill-layer count
  * of the dispatcher (Sec. 3.4).  Host-side only: these calls touch no GPU.

@@ -2,6 +2,7 @@
 // the split kernel (its work-unit body is in decode_block.h), the combine
 // kernel and their launch.
 #include <algorithm>
+#include <mutex>
 
 #include "decode_block.h"
 
@@ -267,22 +268,21 @@ mw_status mw_decode_workspace_size(const mw_attn_shape *shape, int32_t batch, co
     return MW_OK;
 }
 
-mw_status mw_decode_attn(const mw_kv_pool *pool, const mw_attn_shape *shape, int32_t batch,
-                         const int32_t *h_seq_lens, const int32_t *d_seq_lens, const int32_t *d_block_table,
-                         int32_t bt_stride, const void *d_q, void *d_out, void *d_workspace,
-                         size_t workspace_bytes, int32_t chunk_pages, mw_stream stream, mw_timing *timing) {
-    const char *who = "mw_decode_attn";
-    if (!shape) return fail(MW_ERR_INVALID_ARG, "%s: bad arguments", who);
-    const mw_decode_args a{pool,   *shape, batch,        h_seq_lens,      d_seq_lens, d_block_table,
-                           bt_stride, d_q, d_out, d_workspace, workspace_bytes, chunk_pages};
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    DecodePlan pl;
-    mw_status st = decode_prepare(&a, stream_cus(s), &pl, who);
-    if (st != MW_OK) return st;
-    st = timing_begin(timing, s);
+}  // extern "C"
+
+namespace {
+
+// The split and combine launches of one planned decode call.
+mw_status decode_launch(const mw_decode_args &a, const DecodePlan &pl, hipStream_t s, mw_timing *timing) {
+    const mw_kv_pool *pool = a.pool;
+    const int32_t batch = a.batch, bt_stride = a.bt_stride;
+    const int32_t *d_seq_lens = a.d_seq_lens, *d_block_table = a.d_block_table;
+    const void *d_q = a.d_q;
+    void *d_out = a.d_out;
+    mw_status st = timing_begin(timing, s);
     if (st != MW_OK) return st;
     if (pl.units > 0) {
-        char *ws = static_cast<char *>(d_workspace);
+        char *ws = static_cast<char *>(a.d_workspace);
         if (pl.per_unit > 0) {
             hipLaunchKernelGGL(k_decode_balanced, dim3(static_cast<unsigned>(pl.units)), dim3(kThreads), 0, s,
                                pool->k, pool->v, static_cast<const uint16_t *>(d_q), static_cast<uint16_t *>(d_out),
@@ -309,6 +309,84 @@ mw_status mw_decode_attn(const mw_kv_pool *pool, const mw_attn_shape *shape, int
     st = timing_kernel_done(timing, s);
     timing_end(timing);
     return st;
+}
+
+// Workspace of mw_decode_attn_noalloc: one array per device for the whole
+// process, shared by every call on that device.  Host code never uses the
+// array's name as an address (on the host it names a stand-in, not device
+// memory): each device's address comes from hipGetSymbolAddress, taken once
+// per device with that device current.
+constexpr size_t kScratchBytes = size_t{16} << 20;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+mw_status scratch_for_stream(hipStream_t s, void **out, const char *who) {
+    int dev = 0;
+    if (s)
+        MW_HIP_TRY(hipStreamGetDevice(s, &dev));
+    else
+        MW_HIP_TRY(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) return fail(MW_ERR_UNSUPPORTED, "%s: device %d out of range", who, dev);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        int prev = 0;
+        MW_HIP_TRY(hipGetDevice(&prev));
+        if (prev != dev) MW_HIP_TRY(hipSetDevice(dev));
+        void *ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (prev != dev) (void)hipSetDevice(prev);
+        if (e != hipSuccess || !ptr)
+            return fail(MW_ERR_HIP, "%s: hipGetSymbolAddress(scratch) failed: %s", who, hipGetErrorString(e));
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return MW_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+mw_status mw_decode_attn(const mw_kv_pool *pool, const mw_attn_shape *shape, int32_t batch,
+                         const int32_t *h_seq_lens, const int32_t *d_seq_lens, const int32_t *d_block_table,
+                         int32_t bt_stride, const void *d_q, void *d_out, void *d_workspace,
+                         size_t workspace_bytes, int32_t chunk_pages, mw_stream stream, mw_timing *timing) {
+    const char *who = "mw_decode_attn";
+    if (!shape) return fail(MW_ERR_INVALID_ARG, "%s: bad arguments", who);
+    const mw_decode_args a{pool,   *shape, batch,        h_seq_lens,      d_seq_lens, d_block_table,
+                           bt_stride, d_q, d_out, d_workspace, workspace_bytes, chunk_pages};
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    DecodePlan pl;
+    mw_status st = decode_prepare(&a, stream_cus(s), &pl, who);
+    if (st != MW_OK) return st;
+    return decode_launch(a, pl, s, timing);
+}
+
+mw_status mw_decode_attn_noalloc(const mw_kv_pool *pool, const mw_attn_shape *shape, int32_t batch,
+                                 const int32_t *h_seq_lens, const int32_t *d_seq_lens,
+                                 const int32_t *d_block_table, int32_t bt_stride, const void *d_q,
+                                 void *d_out, int32_t chunk_pages, mw_stream stream) {
+    const char *who = "mw_decode_attn_noalloc";
+    if (!shape) return fail(MW_ERR_INVALID_ARG, "%s: bad arguments", who);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    void *ws = nullptr;
+    mw_status st = scratch_for_stream(s, &ws, who);
+    if (st != MW_OK) return st;
+    const mw_decode_args a{pool,      *shape, batch, h_seq_lens, d_seq_lens,    d_block_table,
+                           bt_stride, d_q,    d_out, ws,         kScratchBytes, chunk_pages};
+    // plan with an unbounded workspace first, so that a call too large for
+    // the scratch array is reported as such
+    mw_decode_args sized = a;
+    sized.workspace_bytes = ~size_t{0};
+    DecodePlan pl;
+    st = decode_prepare(&sized, stream_cus(s), &pl, who);
+    if (st != MW_OK) return st;
+    if (pl.bytes > kScratchBytes)
+        return fail(MW_ERR_UNSUPPORTED, "%s: the call needs %zu bytes of workspace, the static scratch holds %zu",
+                    who, pl.bytes, kScratchBytes);
+    return decode_launch(a, pl, s, nullptr);
 }
 
 }  // extern "C"

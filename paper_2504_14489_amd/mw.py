@@ -130,6 +130,7 @@ _SIGNATURES = {
                                   ctypes.POINTER(ctypes.c_size_t)], _I),
     "mw_decode_attn": ([_P, ctypes.POINTER(_AttnShape), _I, _PI, _P, _P, _I, _P, _P, _P,
                         ctypes.c_size_t, _I, _P, _P], _I),
+    "mw_decode_attn_noalloc": ([_P, ctypes.POINTER(_AttnShape), _I, _PI, _P, _P, _I, _P, _P, _I, _P], _I),
     "mw_predictor_create": ([ctypes.POINTER(_P)], _I),
     "mw_predictor_destroy": ([_P], _I),
     "mw_predictor_add_prefill": ([_P, _I, _I, _PI, _PI, ctypes.c_double], _I),
@@ -374,6 +375,16 @@ def mw_decode_attn(pool, num_q_heads: int, num_kv_heads: int, head_dim: int, sca
     _check(load().mw_decode_attn(pool, ctypes.byref(sh), len(sl), _pi(sl), _h(d_seq_lens),
                                  _h(d_block_table), bt_stride, _h(d_q), _h(d_out), _h(d_workspace),
                                  workspace_bytes, chunk_pages, _h(stream), timing))
+
+
+def mw_decode_attn_noalloc(pool, num_q_heads: int, num_kv_heads: int, head_dim: int, scale: float,
+                           seq_lens, d_seq_lens: int, d_block_table: int, bt_stride: int, d_q: int,
+                           d_out: int, chunk_pages: int = 0, stream=0):
+    sl = _i32(seq_lens)
+    sh = _shape(num_q_heads, num_kv_heads, head_dim, scale)
+    _check(load().mw_decode_attn_noalloc(pool, ctypes.byref(sh), len(sl), _pi(sl), _h(d_seq_lens),
+                                         _h(d_block_table), bt_stride, _h(d_q), _h(d_out), chunk_pages,
+                                         _h(stream)))
 
 
 # ---- contention-tolerant estimator (host-side)
