@@ -179,6 +179,25 @@ mw_status mw_cu_probe(int32_t n_blocks, int32_t spin_cycles, uint32_t *d_out,
 mw_status mw_stream_read(const void *d_src, size_t bytes, uint32_t *d_sink, int32_t n_blocks,
                          mw_stream stream, mw_timing *timing);
 
+/* Measurement helpers (not part of the attention path).
+ * mw_cache_flush: reads d_buf past its first 16 KiB on `stream` (bytes a
+ *     multiple of 16 and above 16 KiB, 16-byte aligned) and writes one word
+ *     per work-group (2048) into its first 8 KiB; with bytes >= 512 MiB it
+ *     evicts the L2 caches of the stream's XCDs and the 256 MiB Infinity
+ *     Cache, leaving clean lines only, so the next timed call starts cold.
+ * mw_mfma_peak: n_blocks 256-thread work-groups each issuing `iters` rounds of
+ *     four bf16 32x32x16 MFMAs per wave from registers, on `stream`; *flop
+ *     (may be NULL) receives the launch's floating-point operations and
+ *     d_sink[n_blocks] one folded value per work-group.  Timed with `timing`
+ *     (may be NULL), it measures the matrix-core ceiling of the stream's CUs.
+ * mw_trace_mark: launches an empty kernel (k_trace_mark) of `id` one-wave
+ *     work-groups (1 <= id <= 65536), so that a kernel trace can find marked
+ *     points of a program by that kernel's grid size. */
+mw_status mw_cache_flush(void *d_buf, size_t bytes, mw_stream stream);
+mw_status mw_mfma_peak(int32_t n_blocks, int32_t iters, float *d_sink, mw_stream stream, mw_timing *timing,
+                       double *flop);
+mw_status mw_trace_mark(int32_t id, mw_stream stream);
+
 /* ------------------------------------------------------------------------
  * Per-call timing.  A call given a timing handle records a start event, one
  * event after each kernel it launches, and (implicitly) a stop event = the

@@ -18,7 +18,7 @@ k_decode_split(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ 
                const int32_t *__restrict__ seq_lens, const int32_t *__restrict__ bt, int bt_stride,
                float *__restrict__ ws_o, float2 *__restrict__ ws_ml, int32_t *__restrict__ ws_cbase,
                int batch, int hkv, int group, int num_pages, float scale_log2, int ch_pages) {
-    __shared__ __attribute__((aligned(16))) uint16_t s_v[kWaves * kVBufElems];
+    __shared__ __attribute__((aligned(16))) uint16_t s_v[kWaves * kWaveBufElems];
     __shared__ float s_m[kWaves][16];
     __shared__ float s_l[kWaves][16];
     decode_unit<false>(kpool, vpool, q, out, seq_lens, bt, bt_stride, ws_o, ws_ml, ws_cbase, batch, hkv, group,
@@ -34,7 +34,7 @@ k_decode_balanced(const uint16_t *__restrict__ kpool, const uint16_t *__restrict
                   float *__restrict__ ws_o, float2 *__restrict__ ws_ml, int32_t *__restrict__ ws_cbase,
                   int batch, int hkv, int group, int num_pages, float scale_log2, int64_t per_unit,
                   int64_t total) {
-    __shared__ __attribute__((aligned(16))) uint16_t s_v[kWaves * kVBufElems];
+    __shared__ __attribute__((aligned(16))) uint16_t s_v[kWaves * kWaveBufElems];
     __shared__ float s_m[kWaves][16];
     __shared__ float s_l[kWaves][16];
     decode_span(kpool, vpool, q, out, seq_lens, bt, bt_stride, ws_o, ws_ml, ws_cbase, batch, hkv, group, num_pages,

@@ -11,12 +11,15 @@
 // result does not change when pages are renumbered.
 //
 // Each wave streams its own pages of the chunk two at a time (a "pair"), with
-// the next pair's loads in flight while the current pair is computed:
-//   * K rows are loaded straight into the A operand of a 16x16x32 bf16 MFMA
-//     (one page = 16 tokens x 32 dims per step), B = Q^T of the kv head's G
-//     query heads (columns >= G are zero): S^T[token][head].
-//   * V rows go to a per-wave LDS buffer as loaded (16-byte row-major stores)
-//     and come back through the transposing LDS read as the A operand of a
+// the next pair's loads in flight while the current pair is computed.  K and
+// V rows are loaded whole (each instruction reads four 256-byte rows, so no
+// cache line is requested twice) with streaming loads that leave nothing in
+// the caches for the other partition's kernel to lose, and go to per-wave LDS
+// buffers as loaded (16-byte row-major stores):
+//   * K comes back in the A-operand layout of a 16x16x32 bf16 MFMA (one page
+//     = 16 tokens x 32 dims per step), B = Q^T of the kv head's G query heads
+//     (columns >= G are zero): S^T[token][head].
+//   * V comes back through the transposing LDS read as the A operand of a
 //     second MFMA, O^T[d][head] += V^T[d][token] P^T[token][head]; P^T is the
 //     S^T accumulator itself, converted to bf16.
 //   * online softmax per pair in base 2; the reference maximum moves only
@@ -43,8 +46,11 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kPair = 2;                      // pages per wave step
-constexpr int VSTR = 144;                     // LDS V row stride (bf16): conflict-free
+constexpr int VSTR = 144;                     // LDS V row stride (bf16): conflict-free transposing reads
+constexpr int KSTR = 136;                     // LDS K row stride (bf16): conflict-free 16-byte reads
 constexpr int kVBufElems = 16 * kPair * VSTR; // one wave's V buffer
+constexpr int kKBufElems = 16 * kPair * KSTR; // one wave's K buffer
+constexpr int kWaveBufElems = kVBufElems + kKBufElems;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kRescaleLog2 = 8.f;
 // chunk_pages = 0: the largest of 128, 64, 32 pages that still gives at least
@@ -105,8 +111,15 @@ __device__ bool locate_chunk(const int32_t *__restrict__ seq_lens, int batch, in
     return false;
 }
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+// Streaming load: the line is not kept in the caches (decode reads each byte
+// of K/V once), so the other partition's working set stays there.
+__device__ inline uint4 load_stream(const uint16_t *p) {
+    return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p)));
+}
+
 struct PairRegs {
-    uint4 k[kPair][4];  // K rows as the MFMA A operand: token = lane%16, dims 32kb + 8(lane/16) + 0..7
+    uint4 k[kPair][4];  // K rows as loaded: token 4i + lane/16, dims 8(lane%16) + 0..7
     uint4 v[kPair][4];  // V rows: token 4i + lane/16, dims 8(lane%16) + 0..7
     bool ok[kPair];
 };
@@ -121,14 +134,14 @@ __device__ inline void pair_load(PairRegs &pr, const uint16_t *__restrict__ kpoo
         const int page = btrow[p < p_end ? p : p0];
         pr.ok[j] = p < p_end && page >= 0 && page < num_pages;
         const size_t base = (static_cast<size_t>(pr.ok[j] ? page : 0) * hkv + kvh) * (kPageSize * kHeadDim);
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-            pr.k[j][kb] = *reinterpret_cast<const uint4 *>(kpool + base + (lane & 15) * kHeadDim + 32 * kb +
-                                                          8 * (lane >> 4));
+        // whole 256-byte rows per instruction (four rows each), so no cache
+        // line is requested by two instructions
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-            pr.v[j][i] = *reinterpret_cast<const uint4 *>(vpool + base + (4 * i + (lane >> 4)) * kHeadDim +
-                                                         8 * (lane & 15));
+            pr.k[j][i] = load_stream(kpool + base + (4 * i + (lane >> 4)) * kHeadDim + 8 * (lane & 15));
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            pr.v[j][i] = load_stream(vpool + base + (4 * i + (lane >> 4)) * kHeadDim + 8 * (lane & 15));
     }
 }
 
@@ -164,7 +177,10 @@ decode_pages(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vp
     for (int db = 0; db < 8; ++db) oacc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
     float m_run = -INFINITY, l_run = 0.f;
 
-    uint16_t *vbuf = s_v + wave * kVBufElems;
+    uint16_t *vbuf = s_v + wave * kWaveBufElems;
+    uint16_t *kbuf = vbuf + kVBufElems;
+    // K operand reads: lane l reads row l%16 of each page, 16-byte chunk 4kb + l/16
+    const uint16_t *krd = kbuf + col * KSTR + 8 * grp;
     // transposing-read source: lane s of 16-lane group g -> row 4g + s/4 (+16 for
     // the second page), dims 4(s%4) (+16 db)
     const uint16_t *vtr = vbuf + (4 * grp + (col >> 2)) * VSTR + 4 * (col & 3);
@@ -178,28 +194,33 @@ decode_pages(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vp
         bool ok[kPair];
 #pragma unroll
         for (int j = 0; j < kPair; ++j) ok[j] = pr.ok[j];
-        // V of this pair -> LDS as loaded, with rows of an absent page or past
-        // the sequence's end as zeros (a masked key has p = 0, but 0 times a
-        // NaN or Inf in a slack slot would not be 0); then K -> S^T on the
-        // matrix core (scores of those keys are masked below)
+        // K and V of this pair -> LDS as loaded, with V rows of an absent page
+        // or past the sequence's end as zeros (a masked key has p = 0, but 0
+        // times a NaN or Inf in a slack slot would not be 0); the scores of
+        // those keys are masked below
 #pragma unroll
         for (int j = 0; j < kPair; ++j)
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < 4; ++i) {
+                *reinterpret_cast<uint4 *>(kbuf + (16 * j + 4 * i + grp) * KSTR + 8 * col) = pr.k[j][i];
                 *reinterpret_cast<uint4 *>(vbuf + (16 * j + 4 * i + grp) * VSTR + 8 * col) =
                     sel4(pr.ok[j] && (p0 + j) * kPageSize + 4 * i + grp < L, pr.v[j][i]);
+            }
+        // next pair's loads go out while this pair is computed
+        const int pn = p0 + pstep;
+        if (pn < p_end) pair_load(pr, kpool, vpool, btrow, pn, p_end, hkv, kvh, num_pages);
+        // S^T = K Q^T on the matrix core, K read back in the operand layout
         f32x4 sc[kPair];
 #pragma unroll
         for (int j = 0; j < kPair; ++j) {
             sc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
-                sc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, pr.k[j][kb]),
+            for (int kb = 0; kb < 4; ++kb) {
+                const uint4 a = *reinterpret_cast<const uint4 *>(krd + 16 * j * KSTR + 32 * kb);
+                sc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
                                                                 __builtin_bit_cast(bf16x8, qop[kb]), sc[j], 0, 0, 0);
+            }
         }
-        // next pair's loads go out while this pair is finished
-        const int pn = p0 + pstep;
-        if (pn < p_end) pair_load(pr, kpool, vpool, btrow, pn, p_end, hkv, kvh, num_pages);
 
         // mask keys past the sequence or on an absent page, then the pair's
         // maximum per head

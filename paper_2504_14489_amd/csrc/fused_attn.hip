@@ -24,7 +24,7 @@ constexpr int kPrefillK = 0;
 constexpr int kPrefillV = 2 * pf::TILE * 2;
 constexpr int kPrefillBt = 4 * pf::TILE * 2;
 constexpr int kPrefillBytes = kPrefillBt + pf::kBtCache * 4;
-constexpr int kDecodeV = dk::kWaves * dk::kVBufElems * 2;
+constexpr int kDecodeV = dk::kWaves * dk::kWaveBufElems * 2;
 constexpr int kDecodeHalf = kDecodeV + 2 * dk::kWaves * 16 * 4;
 constexpr int kLdsBytes = kPrefillBytes > 2 * kDecodeHalf ? kPrefillBytes : 2 * kDecodeHalf;
 static_assert(kDecodeHalf % 16 == 0, "decode LDS halves stay 16-byte aligned");

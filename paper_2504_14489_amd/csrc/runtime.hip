@@ -343,3 +343,103 @@ extern "C" mw_status mw_stream_read(const void *d_src, size_t bytes, uint32_t *d
     timing_end(timing);
     return st;
 }
+
+// ----------------------------------------------------------- cache flush ----
+// Reads the buffer past its first 16 KiB once with 16-byte loads: run between
+// isolated timed calls, it evicts what the previous call left in the L2 of
+// every XCD the stream runs on and in the memory-side Infinity Cache, leaving
+// only clean lines (a flush by writing would leave dirty lines whose
+// write-back the next, timed, kernel would pay for).  Each work-group folds
+// what it read into one word of the buffer's first 8 KiB.
+constexpr int kFlushBlocks = 2048;
+constexpr size_t kFlushSkip = 16384;
+
+__global__ void __launch_bounds__(256) k_cache_flush(uint4 *__restrict__ buf, size_t n_vec) {
+    const uint4 *src = buf + kFlushSkip / 16;
+    const size_t stride = static_cast<size_t>(gridDim.x) * blockDim.x;
+    uint32_t acc = 0;
+    size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    for (; i + 3 * stride < n_vec; i += 4 * stride) {
+        uint4 v[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = src[i + j * stride];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc ^= v[j].x ^ v[j].y ^ v[j].z ^ v[j].w;
+    }
+    for (; i < n_vec; i += stride) {
+        const uint4 v = src[i];
+        acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
+    acc = __reduce_or_sync(~0ull, acc);
+    if (threadIdx.x == 0) reinterpret_cast<uint32_t *>(buf)[blockIdx.x] = acc;
+}
+
+extern "C" mw_status mw_cache_flush(void *d_buf, size_t bytes, mw_stream stream) {
+    if (!d_buf || bytes % 16 || !aligned16(d_buf) || bytes <= kFlushSkip)
+        return fail(MW_ERR_INVALID_ARG, "mw_cache_flush: bad arguments");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipLaunchKernelGGL(k_cache_flush, dim3(kFlushBlocks), dim3(256), 0, s, static_cast<uint4 *>(d_buf),
+                       (bytes - kFlushSkip) / 16);
+    return check_launch("k_cache_flush");
+}
+
+// ------------------------------------------------------------ MFMA peak -----
+// Each wave issues `iters` rounds of four independent bf16 32x32x16 MFMAs
+// (32768 flop each) from registers: the matrix-core throughput the CUs of a
+// stream sustain at the clock the chip holds under that load.  The result is
+// folded into d_sink[block] so the products cannot be dropped.
+typedef __bf16 mp_bf16x8 __attribute__((ext_vector_type(8)));
+typedef float mp_f32x16 __attribute__((ext_vector_type(16)));
+
+__global__ void __launch_bounds__(256) k_mfma_peak(float *__restrict__ sink, int iters) {
+    const float x = 1e-3f * static_cast<float>((threadIdx.x & 7) + 1);
+    mp_bf16x8 a, b;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        a[i] = static_cast<__bf16>(x);
+        b[i] = static_cast<__bf16>(x * 0.5f);
+    }
+    mp_f32x16 acc[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[j][i] = 0.f;
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[j], 0, 0, 0);
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) s += acc[j][i];
+    if (threadIdx.x == 0) sink[blockIdx.x] = s;
+}
+
+extern "C" mw_status mw_mfma_peak(int32_t n_blocks, int32_t iters, float *d_sink, mw_stream stream,
+                                  mw_timing *timing, double *flop) {
+    if (n_blocks < 1 || n_blocks > (1 << 20) || iters < 1 || iters > (1 << 24) || !d_sink)
+        return fail(MW_ERR_INVALID_ARG, "mw_mfma_peak: bad arguments");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    mw_status st = timing_begin(timing, s);
+    if (st != MW_OK) return st;
+    hipLaunchKernelGGL(k_mfma_peak, dim3(n_blocks), dim3(256), 0, s, d_sink, iters);
+    st = check_launch("k_mfma_peak");
+    if (st != MW_OK) return st;
+    st = timing_kernel_done(timing, s);
+    timing_end(timing);
+    if (flop) *flop = static_cast<double>(n_blocks) * 4 * static_cast<double>(iters) * 4 * 32768.0;
+    return st;
+}
+
+// ------------------------------------------------------------ trace mark ----
+// An empty kernel of `id` one-wave work-groups: a kernel trace shows it as
+// k_trace_mark with grid size 64 * id, which lets a trace reader find the
+// points where a program marked itself (the start and end of a timed region).
+__global__ void __launch_bounds__(64) k_trace_mark() {}
+
+extern "C" mw_status mw_trace_mark(int32_t id, mw_stream stream) {
+    if (id < 1 || id > (1 << 16)) return fail(MW_ERR_INVALID_ARG, "mw_trace_mark: id must be in [1, 65536]");
+    hipLaunchKernelGGL(k_trace_mark, dim3(id), dim3(64), 0, static_cast<hipStream_t>(stream));
+    return check_launch("k_trace_mark");
+}

@@ -39,7 +39,11 @@ def bits_to_f32(b: np.ndarray) -> np.ndarray:
 class DeviceWorkload:
     """Uploads a :class:`Workload` and registers its pool with the library."""
 
-    def __init__(self, wl: Workload, device: str = "cuda:0", copies: int = 1):
+    def __init__(self, wl: Workload, device: str = "cuda:0", replicas: int = 1):
+        """``replicas`` > 1 uploads that many copies of the K/V pool (same
+        contents, own addresses), each registered as its own pool: a benchmark
+        rotates calls over them so that a working set smaller than the GPU's
+        caches is still read from HBM."""
         self.wl = wl
         self.cfg = wl.cfg
         self.device = torch.device(device)
@@ -48,8 +52,11 @@ class DeviceWorkload:
         self.scale = 1.0 / math.sqrt(c.head_dim)
         self.k_pool = _dev16(wl.k_pool, self.device)
         self.v_pool = _dev16(wl.v_pool, self.device)
-        self.pool = mw.mw_kv_pool_create(wl.num_pages, c.page_size, c.hkv, c.head_dim,
-                                         self.k_pool.data_ptr(), self.v_pool.data_ptr())
+        self.k_pools = [self.k_pool] + [self.k_pool.clone() for _ in range(replicas - 1)]
+        self.v_pools = [self.v_pool] + [self.v_pool.clone() for _ in range(replicas - 1)]
+        self.pools = [mw.mw_kv_pool_create(wl.num_pages, c.page_size, c.hkv, c.head_dim, k.data_ptr(), v.data_ptr())
+                      for k, v in zip(self.k_pools, self.v_pools)]
+        self.pool = self.pools[0]
         self.pre_bt = _dev32(wl.pre_bt[None, :], self.device)
         self.dec_bt = _dev32(wl.dec_bt, self.device)
         self.dec_lens = wl.dec_lens.astype(np.int32)
@@ -62,10 +69,15 @@ class DeviceWorkload:
         self._pre_args = {}
         self._dec_start = None
 
+    @property
+    def replicas(self) -> int:
+        return len(self.pools)
+
     def close(self):
-        if self.pool is not None:
-            mw.mw_kv_pool_destroy(self.pool)
-            self.pool = None
+        for p in self.pools:
+            mw.mw_kv_pool_destroy(p)
+        self.pools = []
+        self.pool = None
 
     # ----------------------------------------------------------- prefill --
     def _prefill_args(self, r: int, n: int):
@@ -102,23 +114,24 @@ class DeviceWorkload:
         return self._ws[chunk_pages]
 
     def decode(self, stream=0, timing=None, chunk_pages: int = 0,
-               out: Optional[torch.Tensor] = None):
+               out: Optional[torch.Tensor] = None, replica: int = 0):
         ws = self.workspace(chunk_pages)
         o = self.o_dec if out is None else out
-        mw.mw_decode_attn(self.pool, self.hq, self.hkv, self.d, self.scale, self.dec_lens,
+        mw.mw_decode_attn(self.pools[replica], self.hq, self.hkv, self.d, self.scale, self.dec_lens,
                           self.d_dec_lens.data_ptr(), self.dec_bt.data_ptr(), self.dec_bt.shape[1],
                           self.q_dec.data_ptr(), o.data_ptr(), ws.data_ptr(), ws.numel(),
                           chunk_pages, stream, timing)
         return o
 
-    def write_decode_kv(self, k_new: torch.Tensor, v_new: torch.Tensor, stream=0, timing=None):
+    def write_decode_kv(self, k_new: torch.Tensor, v_new: torch.Tensor, stream=0, timing=None,
+                        replica: int = 0):
         """Appends each decode sequence's newest token at position L-1."""
         B = len(self.dec_lens)
         if self._dec_start is None:
             self._dec_start = (_dev32(np.arange(B + 1), self.device),
                                _dev32(self.dec_lens - 1, self.device))
         indptr, start = self._dec_start
-        mw.mw_kv_pool_write(self.pool, np.ones(B, np.int32), self.dec_lens - 1,
+        mw.mw_kv_pool_write(self.pools[replica], np.ones(B, np.int32), self.dec_lens - 1,
                             indptr.data_ptr(), start.data_ptr(), self.dec_bt.data_ptr(),
                             self.dec_bt.shape[1], k_new.data_ptr(), v_new.data_ptr(), stream,
                             timing)

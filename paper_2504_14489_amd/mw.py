@@ -116,6 +116,9 @@ _SIGNATURES = {
     "mw_partition_masks": ([_P, _PU, _PU], _I),
     "mw_partition_destroy": ([_P], _I),
     "mw_cu_probe": ([_I, _I, _P, _P, _P], _I),
+    "mw_cache_flush": ([_P, ctypes.c_size_t, _P], _I),
+    "mw_mfma_peak": ([_I, _I, _P, _P, _P, ctypes.POINTER(ctypes.c_double)], _I),
+    "mw_trace_mark": ([_I, _P], _I),
     "mw_stream_read": ([_P, ctypes.c_size_t, _P, _I, _P, _P], _I),
     "mw_timing_create": ([ctypes.POINTER(_P)], _I),
     "mw_timing_destroy": ([_P], _I),
@@ -299,6 +302,21 @@ def mw_partition_destroy(part):
 
 def mw_cu_probe(n_blocks: int, spin_cycles: int, d_out: int, stream=0, timing=None):
     _check(load().mw_cu_probe(n_blocks, spin_cycles, _h(d_out), _h(stream), timing))
+
+
+def mw_cache_flush(d_buf: int, nbytes: int, stream=0):
+    _check(load().mw_cache_flush(_h(d_buf), nbytes, _h(stream)))
+
+
+def mw_mfma_peak(n_blocks: int, iters: int, d_sink: int, stream=0, timing=None) -> float:
+    """Launches the matrix-core probe; returns its floating-point operations."""
+    flop = ctypes.c_double()
+    _check(load().mw_mfma_peak(n_blocks, iters, _h(d_sink), _h(stream), timing, ctypes.byref(flop)))
+    return flop.value
+
+
+def mw_trace_mark(mark_id: int, stream=0):
+    _check(load().mw_trace_mark(mark_id, _h(stream)))
 
 
 def mw_stream_read(d_src: int, nbytes: int, d_sink: int, n_blocks: int, stream=0, timing=None):

@@ -169,11 +169,44 @@ def trace(args):
                 seq = seq[:len(seq) - args.skip_last] if args.skip_last else seq
                 last = seq[-args.trace_last:]
                 lines.append(f"| {k} | {statistics.mean(last) / 1e3:.1f} | {statistics.median(last) / 1e3:.1f} |")
+    if args.regions:
+        lines += marked_regions(args.stats_dir, args.kernels.split(","))
     if args.note:
         lines += ["", args.note]
     with open(args.out, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
+
+
+def marked_regions(d: str, kernels):
+    """Per-kernel durations inside each timed region the benchmark marked:
+    k_trace_mark dispatches of id MARK_BASE + 64 w + 2 p open the region of
+    workload w (bench.ORDER), CU split p on both streams and id + 1 closes it;
+    a kernel belongs to the region when its dispatch starts inside it."""
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    from bench import MARK_BASE, ORDER
+    marks = defaultdict(list)
+    disp = []
+    for r in _rows(d, "kernel_trace.csv"):
+        name = _short(r["Kernel_Name"])
+        t0, t1 = int(r["Start_Timestamp"]), int(r["End_Timestamp"])
+        if name == "k_trace_mark":
+            marks[int(r["Grid_Size_X"]) // int(r["Workgroup_Size_X"])].append((t0, t1))
+        elif name in kernels:
+            disp.append((t0, t1, name))
+    out = ["", "## Timed regions marked by bench.py (dispatches starting between the marks)", "",
+           "| workload | split | kernel | dispatches | mean (us) | median (us) |", "|---|---|---|---|---|---|"]
+    for mid in sorted(marks):
+        if (mid - MARK_BASE) % 2 or mid + 1 not in marks:
+            continue
+        lo, hi = min(t for t, _ in marks[mid]), max(t for _, t in marks[mid + 1])
+        w, p = divmod(mid - MARK_BASE, 64)
+        for k in kernels:
+            ds = [(t1 - t0) / 1e3 for t0, t1, n in disp if n == k and lo <= t0 <= hi]
+            if ds:
+                out.append(f"| {ORDER[w] if w < len(ORDER) else w} | {p // 2} | {k} | {len(ds)} | "
+                           f"{statistics.mean(ds):.1f} | {statistics.median(ds):.1f} |")
+    return out
 
 
 def main(argv=None):
@@ -192,6 +225,7 @@ def main(argv=None):
     k.add_argument("--skip-last", type=int, default=0)
     k.add_argument("--kernels", default="k_prefill_attn,k_decode_balanced")
     k.add_argument("--note", default="")
+    k.add_argument("--regions", action="store_true", help="durations inside the regions bench.py marked")
     k.add_argument("--out", required=True)
     m = sub.add_parser("mfma")
     m.add_argument("--dir", required=True)
