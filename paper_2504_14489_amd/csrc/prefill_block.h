@@ -79,11 +79,6 @@ __device__ inline uint32_t cvt2(float a, float b) {
     return __builtin_bit_cast(uint32_t, v);
 }
 
-__device__ inline float dot2_ones(uint32_t p, float acc) {
-    const bf16x2 one = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
-    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p), one, acc, false);
-}
-
 // NaN-propagating maximum: a single v_maximum3_f32 on gfx950, with no
 // canonicalisation of the MFMA results it reads.
 __device__ inline float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
@@ -256,16 +251,16 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
             goff[j], 0, 0, 0);
     };
 
-    // Matrix work on tile t: O^T += V(t)^T P(t)^T (if PV), then
-    // S(t)^T = K(t) Q^T (if QK); `load(j)` is called after every fourth MFMA.
-    // Operation i < npv is PV key-step i/4, dim block i%4; the rest are QK
-    // dim-step j/2, key block j%2.
-    auto mfma_phase = [&](auto pv_flag, auto qk_flag, int t, auto load) __attribute__((always_inline)) {
+    // Matrix work: O^T += V^T P^T with V from tile buffer vbuf (if PV), then
+    // S^T = K Q^T with K from tile buffer kbuf (if QK); `load(j)` is called
+    // after every kEvery-th MFMA of a QK-only phase.  Operation i < npv is PV
+    // key-step i/4, dim block i%4; the rest are QK dim-step j/2, key block j%2.
+    auto mfma_phase = [&](auto pv_flag, auto qk_flag, int kbuf, int vbuf, auto load) __attribute__((always_inline)) {
         constexpr bool PV = decltype(pv_flag)::value, QK = decltype(qk_flag)::value;
         constexpr int npv = PV ? 16 : 0;
         constexpr int nop = npv + (QK ? 16 : 0);
-        const char *vb_ = reinterpret_cast<const char *>(s_v + (t & 1) * TILE);
-        const char *kb_ = reinterpret_cast<const char *>(s_k + (t & 1) * TILE);
+        const char *vb_ = reinterpret_cast<const char *>(s_v + vbuf * TILE);
+        const char *kb_ = reinterpret_cast<const char *>(s_k + kbuf * TILE);
         // per-read offsets are recomputed here (one XOR each) rather than held
         // in registers across the loop
         int ko = koff, vo0 = voff[0], vo1 = voff[1];
@@ -282,12 +277,6 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
             const int j = i - npv;
             return *reinterpret_cast<const bf16x8 *>(kb_ + (j & 1) * 32 * 256 + (ko ^ (32 * (j >> 1))));
         };
-        if constexpr (QK) {
-#pragma unroll
-            for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) sacc[blk][i] = 0.f;
-        }
         __builtin_amdgcn_s_setprio(2);  // a wave issuing MFMAs wins issue conflicts on the SIMD
         bf16x8 opnd[kAhead];
 #pragma unroll
@@ -300,9 +289,12 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
                 oacc[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                     a, __builtin_bit_cast(bf16x8, pop[i >> 2]), oacc[i & 3], 0, 0, 0);
             } else {
+                // the first step of each key block starts from zero, so the
+                // score registers are free until the QK half of the phase
                 const int j = i - npv;
+                const f32x16 zero = {};
                 sacc[j & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                    a, __builtin_bit_cast(bf16x8, qop[j >> 1]), sacc[j & 1], 0, 0, 0);
+                    a, __builtin_bit_cast(bf16x8, qop[j >> 1]), j < 2 ? zero : sacc[j & 1], 0, 0, 0);
             }
             if (i + kAhead < nop) opnd[i % kAhead] = fetch(i + kAhead);
             if (!PV && i % kEvery == kEvery - 1) load(i / kEvery);
@@ -352,23 +344,25 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
 #pragma unroll
             for (int e = 0; e < 8; ++e) p[e] = __builtin_amdgcn_exp2f(fmaf(sacc[blk][a8 + e], scale_log2, -m_run));
             pop[kstep] = make_uint4(cvt2(p[0], p[1]), cvt2(p[2], p[3]), cvt2(p[4], p[5]), cvt2(p[6], p[7]));
-            // sums of the bf16 values the PV product uses
-            lsum[kstep] = dot2_ones(pop[kstep].w, dot2_ones(pop[kstep].z,
-                                    dot2_ones(pop[kstep].y, dot2_ones(pop[kstep].x, 0.f))));
+            // row sums in fp32 with plain adds: a dot product over the bf16
+            // values would wait behind the other wave's MFMAs on this SIMD
+            lsum[kstep] = ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
         }
         l_run += (lsum[0] + lsum[1]) + (lsum[2] + lsum[3]);
     };
 
     // The first tile of an item: its pages straight from the block table in
-    // HBM, so the loads can start before the table copy in LDS is complete.
-    auto first_tile = [&]() __attribute__((always_inline)) {
+    // HBM, so the loads can start before the table copy in LDS is complete
+    // (its K and, unless the V loads follow one phase later, its V).
+    auto first_tile = [&](auto with_v) __attribute__((always_inline)) {
         const PageRef ref = page_ref(lpage, lpage < np_seq ? btrow[lpage] : -1);
         const __amdgpu_buffer_rsrc_t rk = page_rsrc(kpool, ref), rv = page_rsrc(vpool, ref);
 #pragma unroll
         for (int j = 0; j < kJ; ++j) {
             page_load(rk, s_k, j);
-            page_load(rv, s_v, j);
+            if constexpr (decltype(with_v)::value) page_load(rv, s_v, j);
         }
+        return ref;
     };
 
     for (int item = 0; item < n_items; ++item) {
@@ -378,7 +372,7 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
         qabs = r + pos;
         diag = r + qblk * kBM + (wave >> 2) * 32;  // smallest query of the wave
         if (item > 0) wg_barrier();  // the previous item's output staging is done
-        first_tile();
+        PageRef ref_t = first_tile(flag<NW == 4>());
         // Q^T operand, all 8 dim-steps (k = 16*kb + 8*g + e)
         {
             const bool ok = active && pos < n;
@@ -397,6 +391,69 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
         __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
         wg_barrier();
 
+        if constexpr (NW == 8) {
+            // Two groups of four waves (one wave of each on every SIMD), half a
+            // period apart: while one group runs its matrix phase M(t) =
+            // O += V(t-1)^T P(t-1)^T, S(t) = K(t) Q^T, the other runs the
+            // softmax of its previous scores on the vector ALU, so the matrix
+            // cores of a SIMD stay busy through both waves' softmax.  Period t
+            // (t = 0 .. nt):
+            //   phase 2t:   group 0 M(t)        | group 1 softmax(t-1)
+            //   phase 2t+1: group 0 softmax(t)  | group 1 M(t)
+            // with a work-group barrier after each phase.  K(t+1) and V(t) are
+            // loaded during period t (into the buffers K(t-1) and V(t-2) used)
+            // and waited for at its end.  Row sums are plain fp32 adds: a dot
+            // product instruction would wait behind the other group's MFMAs.
+            const int grp = wave >> 2;
+            // Each wave runs its own sequence M(0) S(0) M(1) .. S(nt-1) M(nt),
+            // group 1 one phase after group 0 (a barrier ends every phase, 2nt+2
+            // in all for both groups).  The loads of period t go out at its
+            // first phase (group 0: before M(t); group 1: before S(t-1)) and
+            // are waited for at its last (group 0: after S(t); group 1: after
+            // M(t)).
+            auto period_loads = [&](int t) __attribute__((always_inline)) {
+                const PageRef ref_n = t + 1 < nt ? tile_page(t + 1) : PageRef{0, 0};
+                if (t + 1 < nt) {
+                    const __amdgpu_buffer_rsrc_t rk = page_rsrc(kpool, ref_n);
+#pragma unroll
+                    for (int j = 0; j < kJ; ++j) page_load(rk, s_k + ((t + 1) & 1) * TILE, j);
+                }
+                if (t < nt) {
+                    const __amdgpu_buffer_rsrc_t rv = page_rsrc(vpool, ref_t);
+#pragma unroll
+                    for (int j = 0; j < kJ; ++j) page_load(rv, s_v + (t & 1) * TILE, j);
+                }
+                ref_t = ref_n;
+            };
+            auto vm_wait = [&]() __attribute__((always_inline)) { __builtin_amdgcn_s_waitcnt(0x0F70); };
+            if (grp == 1) {  // group 1's first phase: none of its own work
+                period_loads(0);
+                wg_barrier();
+            }
+            if (grp == 0) period_loads(0);
+            if (active) mfma_phase(flag<false>(), flag<true>(), 0, 0, [](int) {});  // M(0): S(0) = K(0) Q^T
+            if (grp == 1) vm_wait();
+            wg_barrier();
+            for (int t = 0; t + 1 < nt; ++t) {
+                if (grp == 1) period_loads(t + 1);
+                if (active) softmax_phase(t);
+                if (grp == 0) vm_wait();
+                wg_barrier();
+                if (grp == 0) period_loads(t + 1);
+                if (active)  // M(t+1): O += V(t)^T P(t)^T, S(t+1) = K(t+1) Q^T
+                    mfma_phase(flag<true>(), flag<true>(), (t + 1) & 1, t & 1, [](int) {});
+                if (grp == 1) vm_wait();
+                wg_barrier();
+            }
+            // the last tile: softmax(nt-1), then M(nt) = O += V(nt-1)^T P(nt-1)^T
+            if (active) softmax_phase(nt - 1);
+            if (grp == 0) vm_wait();
+            wg_barrier();
+            if (active) mfma_phase(flag<true>(), flag<false>(), 0, (nt - 1) & 1, [](int) {});
+            if (grp == 1) vm_wait();
+            wg_barrier();
+            if (grp == 0) wg_barrier();  // group 0's last phase: none of its own work
+        } else
         // Tile t+1 is loaded (into the other buffer) while tile t is processed;
         // the K and V pages of a tile are the same pages of the pool.
         for (int t = 0; t < nt; ++t) {
@@ -414,9 +471,9 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
                 }
             };
             if (active) {
-                mfma_phase(flag<false>(), flag<true>(), t, load);
+                mfma_phase(flag<false>(), flag<true>(), t & 1, t & 1, load);
                 softmax_phase(t);
-                mfma_phase(flag<true>(), flag<false>(), t, [](int) {});
+                mfma_phase(flag<true>(), flag<false>(), t & 1, t & 1, [](int) {});
             } else {
 #pragma unroll
                 for (int j = 0; j < 2 * kJ; ++j) load(j);
