@@ -471,7 +471,7 @@ typedef struct {
     int32_t switched_layers;              /* prefill layers run on the whole device */
 } mw_engine_stats;
 /* One launch covering a prefill call and a decode call on the same pool: the
- * fused comparator (paper Sec. 5: the chunked-prefill baseline runs prefill
+ * fused comparator (paper Sec. 4.1: the chunked-prefill baseline runs prefill
  * and decode attention in one kernel on the whole GPU).  Each work-group of
  * the fused kernel is either one prefill work-group or two decode work
  * units; the two kinds are interleaved in dispatch order in proportion to

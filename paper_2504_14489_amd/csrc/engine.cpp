@@ -105,15 +105,24 @@ mw_status check_args(const mw_engine *eng, const mw_decode_args *dec, const mw_p
     return MW_OK;
 }
 
+// Cache key of a decode graph: the decode arguments field by field (never the
+// struct's bytes, whose padding a caller need not initialise), the lengths'
+// values rather than where the host keeps them, and the layer count.
 std::vector<unsigned char> graph_key(const mw_decode_args *dec, int layers) {
-    std::vector<unsigned char> k(sizeof(mw_decode_args) + sizeof(int) +
-                                 sizeof(int32_t) * static_cast<size_t>(std::max(dec->batch, 0)));
-    mw_decode_args a = *dec;
-    a.h_seq_lens = nullptr;     // the lengths' values matter, not where the host keeps them
-    std::memcpy(k.data(), &a, sizeof a);
-    std::memcpy(k.data() + sizeof a, &layers, sizeof layers);
-    if (dec->batch > 0 && dec->h_seq_lens)
-        std::memcpy(k.data() + sizeof a + sizeof layers, dec->h_seq_lens, sizeof(int32_t) * dec->batch);
+    std::vector<unsigned char> k;
+    auto put = [&k](const void *p, size_t n) {
+        const unsigned char *b = static_cast<const unsigned char *>(p);
+        k.insert(k.end(), b, b + n);
+    };
+    const void *ptrs[6] = {dec->pool, dec->d_seq_lens, dec->d_block_table, dec->d_q, dec->d_out, dec->d_workspace};
+    put(ptrs, sizeof ptrs);
+    const int32_t ints[6] = {dec->shape.num_q_heads, dec->shape.num_kv_heads, dec->shape.head_dim, dec->batch,
+                             dec->bt_stride, dec->chunk_pages};
+    put(ints, sizeof ints);
+    put(&dec->shape.scale, sizeof dec->shape.scale);
+    put(&dec->workspace_bytes, sizeof dec->workspace_bytes);
+    put(&layers, sizeof layers);
+    if (dec->batch > 0 && dec->h_seq_lens) put(dec->h_seq_lens, sizeof(int32_t) * static_cast<size_t>(dec->batch));
     return k;
 }
 

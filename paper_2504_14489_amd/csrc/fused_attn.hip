@@ -1,6 +1,6 @@
 // One launch covering a prefill batch and a decode batch: the fused
 // comparator for spatial multiplexing.  Chunked-prefill systems run both
-// attentions in one kernel over the whole GPU (paper Sec. 5, the SGLang
+// attentions in one kernel over the whole GPU (paper Sec. 4.1, the SGLang
 // chunked-prefill baseline with its fused prefill + decode attention); here
 // that is a kernel whose work-groups are either a prefill work-group (the
 // body of the prefill kernel) or two decode work units (the body of the
