@@ -19,7 +19,7 @@ the CU-partition sweep with its contention table, and the long-context 8B
 layer, which carries the headline: the largest single-GPU workload).  For each:
 
 * isolated per-call latency of each phase on its own CUs, with the L2 and
-  Infinity Cache flushed before every timed call (512 MiB written on the same
+  Infinity Cache flushed before every timed call (512 MiB read on the same
   stream), and on the whole GPU; K/V pool replicas rotated per decode call
   when the decode working set is under 512 MB, so it is read from HBM;
 * the multiplexed timed region (per-kernel HIP events on each kernel's own
