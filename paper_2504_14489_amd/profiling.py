@@ -118,7 +118,7 @@ def pair_slowdown(pre: PrefillCall, dec: DecodeCall, part: Partition, pre_ms: fl
     them (decode enqueued first); the decode calls that ran entirely inside
     the prefill window give the multiplexed latency."""
     n_pre = min(256, max(1, math.ceil(3 * dec_ms / pre_ms)))
-    n_dec = math.ceil(n_pre * pre_ms / dec_ms) + 3
+    n_dec = min(512, math.ceil(n_pre * pre_ms / dec_ms) + 3)
     td = [Timing() for _ in range(n_dec)]
     tp = [Timing() for _ in range(n_pre)]
     torch.cuda.synchronize()
@@ -167,15 +167,17 @@ def write_table(result, path, command):
              "Command (on the MI355X box):", "", f"    {command}", "",
              f"Model shape: {m['num_q_heads']} query heads, {m['num_kv_heads']} kv heads, head_dim {m['head_dim']}, "
              f"{m['page_size']}-token pages; random bf16 K/V and Q on the device.",
-             f"Grid (powers of 4, as the paper samples; scaled to one GPU): prefill new tokens {g['prefill_new']}, "
-             f"reused {g['prefill_reused']}; decode batch {g['decode_batch']} with every sequence of length "
-             f"{g['decode_len']}; prefill/decode CUs " + ", ".join(f"{p}/{256 - p}" for p in pcus) + ".  "
+             f"Predictor grid: prefill new tokens {g['prefill_new']}, reused {g['prefill_reused']}; decode batch "
+             f"{g['decode_batch']} with every sequence of length {g['decode_len']} (at most "
+             f"{g.get('max_decode_tokens', 0)} tokens per batch); prefill/decode CUs "
+             + ", ".join(f"{p}/{256 - p}" for p in pcus) + ".  "
              f"Held-out samples: {held} random prefill (n, r) and {held} random decode batches (random lengths per "
              "sequence) per partition.  Solo = median of the calls alone on the partition's CUs; decode = whole "
              "call (split + combine kernels, balanced split).", "",
              "## Solo-run predictor (Eqs. (1)-(2), least squares of the relative error)", "",
-             "| phase | CUs | theta (ms per unit) | max deviation, grid (train) | max deviation, held out |",
-             "|---|---|---|---|---|"]
+             "| phase | CUs | theta (ms per unit) | max deviation, grid (train) | max deviation, held out | "
+             "held out, calls with a work-group per CU |",
+             "|---|---|---|---|---|---|"]
     for phase, cus_list in (("prefill", pcus), ("decode", dcus)):
         nth = 4 if phase == "prefill" else 3
         for c in cus_list:
@@ -183,15 +185,20 @@ def write_table(result, path, command):
                 else result["predictor"][phase][c]
             th = ", ".join(f"{x:.3g}" for x in e["theta"][:nth])
             lines.append(f"| {phase} | {c} | {th} | {100 * e['max_dev']['train']:.1f}% | "
-                         f"{100 * e['max_dev']['held_out']:.1f}% |")
+                         f"{100 * e['max_dev']['held_out']:.1f}% | "
+                         f"{100 * e['max_dev'].get('held_out_filling', float('nan')):.1f}% |")
     lines += ["", "For comparison, the paper's predictor misses whole-model iterations on NVIDIA GPUs by at most "
               "8.16% (prefill) and 8.84% (decode).  Single attention calls keep the step changes of a launch "
-              "(rounds of work-groups over the partition's CUs, paired or single query blocks), which "
-              "linear-in-work models miss, most on 192 CUs."]
+              "(rounds of work-groups over the partition's CUs, paired or single query blocks, and calls whose "
+              "few work-groups all run at once, bound by the longest), which linear-in-work models miss, most on "
+              "large partitions."]
     gd = result["guard"]
+    gg = g.get("guard", g)
     sl = sorted(s["slowdown"] for s in result["pairs"] if s["slowdown"] is not None)
     p90 = sl[int(0.9 * (len(sl) - 1))] if sl else float("nan")
     lines += ["", "## Contention guard (decode slowdown = multiplexed / solo call latency on the same CUs)", "",
+              f"Pairs: every prefill call (new tokens {gg['prefill_new']}, reused {gg['prefill_reused']}) next to "
+              f"every decode batch (batch {gg['decode_batch']} of length {gg['decode_len']}) on each partition.  "
               f"{gd['pairs']} pairs, {gd['pairs_measured']} measured; slowdown median "
               f"{gd['median_slowdown']:.3f}, 90th percentile {p90:.3f}, maximum {gd['max_slowdown']:.3f} "
               "(the paper measures up to 20% on A100 and 30% on H100).", "",
@@ -249,28 +256,43 @@ def fit_and_score(samples, train_filter, phase):
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--out", required=True)
-    ap.add_argument("--prefill-cus", default="64,128,192")
+    ap.add_argument("--prefill-cus", default="32,64,96,128,160,192,224")
     ap.add_argument("--reps", type=int, default=5)
-    ap.add_argument("--held-out", type=int, default=10, help="random held-out samples per partition and phase")
+    ap.add_argument("--held-out", type=int, default=20, help="random held-out samples per partition and phase")
+    ap.add_argument("--guard-reused", default="0,4096,16384,65536",
+                    help="prefill reused tokens of the contention-guard pairs")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--quick", action="store_true", help="a small grid (functional check)")
     ap.add_argument("--table", default="", help="also write the Markdown summary here")
     args = ap.parse_args(argv)
     torch.cuda.init()
-    grid_n = [1024, 4096, 16384]
-    grid_r = [0, 4096, 16384]
-    grid_bs = [8, 32, 128]
-    grid_L = [1024, 4096, 16384]
+    # the predictor's grid: powers of 2 in new tokens and batch size, powers
+    # of 4 in reused tokens and context; the contention guard's pairs take the
+    # powers of 4 (the paper's grid) within it
+    grid_n = [256, 512, 1024, 2048, 4096, 8192, 16384]
+    grid_r = [0, 1024, 4096, 16384, 65536]
+    grid_bs = [1, 2, 4, 8, 16, 32, 64, 128, 256]
+    grid_L = [256, 1024, 4096, 16384, 65536]
+    guard_n = [1024, 4096, 16384]
+    guard_r = [int(x) for x in args.guard_reused.split(",")]
+    guard_bs = [8, 32, 128]
+    guard_L = [1024, 4096, 16384, 65536]
+    max_dec_tokens = 2 ** 22          # decode samples hold at most this many cached tokens (16 GB of K/V)
     if args.quick:
         grid_n, grid_r, grid_bs, grid_L = [128, 512, 1024], [0, 1024], [4, 16], [512, 2048]
+        guard_n, guard_r, guard_bs, guard_L = grid_n, grid_r, grid_bs, grid_L
+        max_dec_tokens = 2 ** 16
     rng = np.random.default_rng(args.seed)
-    pages = grid_bs[-1] * grid_L[-1] // PAGE + (grid_n[-1] + grid_r[-1]) // PAGE + 64
+    pages = max_dec_tokens // PAGE + (grid_n[-1] + grid_r[-1]) // PAGE + 64
     t_start = time.time()
     pool = Pool(pages, args.seed)
     log(f"[profiling] pool of {pages} pages ({2 * pages * HKV * PAGE * D * 2 / 1e9:.1f} GB)")
     result = {"model": {"num_q_heads": HQ, "num_kv_heads": HKV, "head_dim": D, "page_size": PAGE},
               "grid": {"prefill_new": grid_n, "prefill_reused": grid_r, "decode_batch": grid_bs,
-                       "decode_len": grid_L}, "prefill": [], "decode": [], "pairs": []}
+                       "decode_len": grid_L, "max_decode_tokens": max_dec_tokens,
+                       "guard": {"prefill_new": guard_n, "prefill_reused": guard_r, "decode_batch": guard_bs,
+                                 "decode_len": guard_L}},
+              "prefill": [], "decode": [], "pairs": []}
     try:
         for pc in [int(x) for x in args.prefill_cus.split(",")]:
             dc = 256 - pc
@@ -284,19 +306,25 @@ def main(argv=None):
                     c = PrefillCall(pool, n, r)
                     ms = solo_ms(c, part.prefill_stream, args.reps, kernel_only=True)
                     result["prefill"].append({"cus": pc, "n": n, "r": r, "ms": ms, "grid": grid})
-                    if grid:
+                    if grid and n in guard_n and r in guard_r:
                         pre_calls[(n, r)] = (c, ms)
-                dec_pts = [([L] * bs, True) for bs in grid_bs for L in grid_L]
+                dec_pts = [([L] * bs, True) for bs in grid_bs for L in grid_L if bs * L <= max_dec_tokens]
                 for _ in range(args.held_out):
-                    bs = int(rng.integers(grid_bs[0] // 2, grid_bs[-1] * 3 // 4 + 1))  # fits the pool
-                    dec_pts.append((rng.integers(grid_L[0] // 2, grid_L[-1] + 1, bs).tolist(), False))
+                    while True:  # random batches of random lengths that fit the pool
+                        bs = int(rng.integers(1, grid_bs[-1] + 1))
+                        lens = rng.integers(grid_L[0] // 2, grid_L[-1] + 1, bs)
+                        if lens.sum() <= max_dec_tokens:
+                            break
+                    dec_pts.append((lens.tolist(), False))
                 dec_calls = {}
                 for lens, grid in dec_pts:
                     c = DecodeCall(pool, lens)
                     ms = solo_ms(c, part.decode_stream, args.reps, kernel_only=False)
                     result["decode"].append({"cus": dc, "lens": [int(x) for x in lens], "ms": ms, "grid": grid})
-                    if grid:
+                    if grid and len(lens) in guard_bs and lens[0] in guard_L:
                         dec_calls[(len(lens), lens[0])] = (c, ms)
+                    else:
+                        del c
                 log(f"[profiling] {pc}/{dc}: solo runs done ({time.time() - t_start:.0f}s)")
                 for (n, r), (pcall, pms) in pre_calls.items():
                     for (bs, L), (dcall, dms) in dec_calls.items():
