@@ -236,7 +236,9 @@ class Bench:
                 self.gpu.flush(stream)
                 self.dw.decode(stream, tks[i][0].h, replica=rep)
         torch.cuda.synchronize()
-        out = {"k0": [sum(tk.kernel_ms(0) for tk in row) for row in tks],
+        out = {"k0": [sum(tk.all_kernels_ms() if which == "prefill" else tk.kernel_ms(0) for tk in row)
+                      for row in tks],
+               "kernels": tks[-1][0].kernels(),
                "call": [sum(tk.elapsed()[0] for tk in row) for row in tks]}
         if which == "decode":
             out["k1"] = [row[0].kernel_ms(1) for row in tks]
@@ -268,7 +270,8 @@ class Bench:
             torch.cuda.synchronize()
         ref = td[0][0].h
         return {"wall_s": wall,
-                "prefill_k": [sum(t.kernel_ms(0) for t in tp[k]) for k in range(steps)],
+                "prefill_k": [sum(t.all_kernels_ms() for t in tp[k]) for k in range(steps)],
+                "prefill_kernels": tp[0][0].kernels(),
                 "decode_k0": [t.kernel_ms(0) for k in range(steps) for t in td[k]],
                 "decode_call": [t.elapsed()[0] for k in range(steps) for t in td[k]],
                 "prefill_window_ms": [min(mw.mw_timing_offsets(tp[k][0].h, ref)[0] for k in range(steps)),
@@ -345,7 +348,7 @@ def committed_traffic(kernel, workload):
     summary, scaled by the copy-kernel calibration it records; None when the
     summary is missing or the kernel's source has changed since."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
-    if not os.path.exists(path):
+    if kernel not in KERNEL_SOURCES or not os.path.exists(path):
         return None
     vals = {}
     for line in open(path):
@@ -366,7 +369,9 @@ def roofline_entries(b, res):
     n_launch = len(b.chunks)
     pre_ms = res["mux"]["prefill_kernel_ms"] / n_launch
     dec_ms = res["mux"]["decode_split_ms"]
-    pre = {"kernel": "k_prefill_attn", "bound": "mfma", "unit": "TFLOP/s",
+    split = res["mux"]["prefill_kernels"] > 1   # key-range split: split + merge kernels per call
+    pre = {"kernel": "k_prefill_split+k_prefill_merge" if split else "k_prefill_attn", "bound": "mfma",
+           "unit": "TFLOP/s",
            "achieved": b.pre_flop / n_launch / (pre_ms * 1e-3) / 1e12, "peak": BF16_PEAK_TFLOPS,
            "work_per_launch": b.pre_flop / n_launch, "work_unit": "FLOP", "kernel_ms": pre_ms,
            "launches_per_step": n_launch}
@@ -436,6 +441,7 @@ def run_partition(b, p_cus, d_cus, p_index, args):
                 "flushed": True},
         "solo_full_gpu": {"prefill_kernel_ms": median(solo_p["k0"]), "decode_call_ms": median(solo_d["call"])},
         "mux": {"prefill_kernel_ms": median(mux["prefill_k"]), "prefill_kernel_p90_ms": p90(mux["prefill_k"]),
+                "prefill_kernels": mux["prefill_kernels"],
                 "decode_split_ms": median(mux["decode_k0"]), "decode_call_ms": median(mux["decode_call"]),
                 "decode_call_p90_ms": p90(mux["decode_call"]),
                 "prefill_window_ms": mux["prefill_window_ms"], "decode_window_ms": mux["decode_window_ms"]},
@@ -594,7 +600,7 @@ def tables(entries):
             "|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
     for e in entries.values():
         r = e["partitions"][0]
-        pre = r["roofline"] if r["roofline"]["kernel"] == "k_prefill_attn" else r["roofline_other"]
+        pre = r["roofline"] if r["roofline"]["bound"] == "mfma" else r["roofline_other"]
         dec = r["roofline_other"] if pre is r["roofline"] else r["roofline"]
         rows.append(f"| {e['name']} | {r['prefill_cus']}/{r['decode_cus']} | {pre['kernel_ms']:.3f} ms | "
                     f"{pre['achieved']:.1f} | {100 * pre['frac_share']:.1f} | {100 * pre['frac_ceiling']:.1f} | "
@@ -614,7 +620,7 @@ def sweep_table(e):
             "decode iso / mux ms | slowdown | GB/s (mux) | % stream ceiling | % share |",
             "|---|---|---|---|---|---|---|---|---|---|---|"]
     for r in e["partitions"]:
-        pre = r["roofline"] if r["roofline"]["kernel"] == "k_prefill_attn" else r["roofline_other"]
+        pre = r["roofline"] if r["roofline"]["bound"] == "mfma" else r["roofline_other"]
         dec = r["roofline_other"] if pre is r["roofline"] else r["roofline"]
         rows.append(f"| {r['prefill_cus']} | {r['iso']['prefill_kernel_ms']:.3f} / {r['mux']['prefill_kernel_ms']:.3f} | "
                     f"{r['slowdown']['prefill']:.3f} | {pre['achieved']:.1f} | {100 * pre['frac_share']:.1f} | "

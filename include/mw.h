@@ -250,6 +250,38 @@ mw_status mw_prefill_attn(const mw_kv_pool *pool, const mw_attn_shape *shape, in
                           const int32_t *d_block_table, int32_t bt_stride, const void *d_q,
                           void *d_out, mw_stream stream, mw_timing *timing);
 
+/* Prefill with a key-range split for grids too small to fill the stream's
+ * CUs (the launches that run 32-position query blocks, two work-groups per
+ * CU: a lone prefill on the whole device, a tensor-parallel head shard on a
+ * partition).  There the longest causal block (its keys 0 .. r + i) sets the
+ * call's time; the split cuts each block's key range into up to 8 equal
+ * pieces so that the pieces fill about three rounds of the stream's
+ * work-group slots, each piece computes the partial softmax state (reference
+ * maximum m, row sum l, unnormalised output) of its keys into the workspace,
+ * and a second kernel merges the pieces of every split block with the
+ * log-sum-exp identity (the decode combine's merge; Table "tab:theory_cost"
+ * fixes every row's key set, so the merged result is the same attention).
+ * Without a split to make (a grid that fills the CUs, or blocks of at most
+ * 4 key tiles) this is mw_prefill_attn: one launch, workspace unused.  With
+ * one, two launches (split, merge), recorded as two kernels in `timing`.
+ * The split depends on the lengths and on the stream's CU count, never on
+ * page ids; rounding may differ from mw_prefill_attn in the last bits.
+ *
+ * Workspace bytes a call with these lengths may need on a stream of
+ * num_cus CUs (0: the most any stream can need):
+ *     pieces x sum(n) x num_q_heads x (128 x 4 + 8) */
+mw_status mw_prefill_workspace_size(const mw_attn_shape *shape, int32_t batch, const int32_t *h_new_lens,
+                                    const int32_t *h_prefix_lens, int32_t num_cus, size_t *bytes);
+/* Arguments as mw_prefill_attn, plus d_workspace (device, 16-B aligned,
+ * caller-owned, contents need not be initialised) of workspace_bytes.
+ * MW_ERR_INVALID_ARG if the split this call makes needs more workspace than
+ * given (the size call with this stream's CU count, or with 0, suffices). */
+mw_status mw_prefill_attn_ws(const mw_kv_pool *pool, const mw_attn_shape *shape, int32_t batch,
+                             const int32_t *h_new_lens, const int32_t *h_prefix_lens,
+                             const int32_t *d_qo_indptr, const int32_t *d_prefix_lens,
+                             const int32_t *d_block_table, int32_t bt_stride, const void *d_q, void *d_out,
+                             void *d_workspace, size_t workspace_bytes, mw_stream stream, mw_timing *timing);
+
 /* Decode streams each (sequence, kv head) segment of the K/V pages split into
  * pieces whose partial results a second kernel merges (log-sum-exp combine,
  * the flash-decoding split of Sec. 2.2's memory-bound decode).  chunk_pages

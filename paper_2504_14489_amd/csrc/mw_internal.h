@@ -21,6 +21,25 @@ mw_status fail(mw_status st, const char *fmt, ...) __attribute__((format(printf,
 
 inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// Key-range split of the prefill query blocks of the 4-wave kernel: a block
+// whose causal key range spans nt tiles of 64 keys is cut into this many
+// pieces, piece i covering tiles [i nt / k, (i + 1) nt / k).  With
+// piece_tiles >= 4 every cut lies at least two tiles before the block's end,
+// so the first tile of every piece holds a key that every query of the block
+// sees (a block's last two tiles hold its diagonal).
+constexpr int kPrefillMaxPieces = 8;
+constexpr int kPrefillMinPieceTiles = 4;
+__host__ __device__ inline int prefill_pieces(int nt, int piece_tiles, int max_pieces) {
+    const int k = (nt + piece_tiles - 1) / piece_tiles;
+    return k < 1 ? 1 : (k > max_pieces ? max_pieces : k);
+}
+// Key tiles (64 keys) of the 32-position query block q of a sequence with
+// prefix r and n new tokens.
+__host__ __device__ inline int prefill_block_tiles(int r, int n, int q) {
+    const int end = 32 * q + 32 < n ? 32 * q + 32 : n;
+    return (r + end + 63) / 64;
+}
+
 // Number of CUs a stream's kernels may run on (its CU mask; all CUs of the
 // current device for a stream without one).
 int stream_cus(hipStream_t s);
@@ -100,10 +119,20 @@ struct PrefillPlan {
     int batch;
     bool table_in_lds;    // every block-table entry a work-group needs fits its LDS copy
     float scale_log2;
+    // key-range split (4-wave blocks only; planned by prefill_split_plan)
+    int pieces;           // most pieces of any block; 1: no split
+    int piece_tiles;      // target key tiles per piece
+    int64_t rows;         // sum of the new lengths (rows of the workspace partials)
+    size_t split_bytes;   // workspace the split needs
 };
 // Validates a prefill call's arguments and plans it for a stream that may use
 // `cus` CUs (block pairing and, with allow_small, the work-group size depend
 // on it).
 mw_status prefill_prepare(const mw_prefill_args *a, int64_t cus, bool allow_small, PrefillPlan *p, const char *who);
+// Plans the key-range split of a 4-wave call on `cus` CUs (cus = 0: the
+// largest split any stream could take); fills pieces, piece_tiles, rows and
+// split_bytes.  Lengths must have been validated.
+void prefill_split_plan(int32_t batch, const int32_t *h_new_lens, const int32_t *h_prefix_lens, int hq,
+                        int64_t cus, PrefillPlan *p);
 
 }  // namespace mw

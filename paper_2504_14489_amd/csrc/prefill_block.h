@@ -70,6 +70,17 @@ constexpr int kAhead = 4;                    // MFMA operands kept in flight
 template <bool B>
 using flag = std::integral_constant<bool, B>;
 
+// Where a piece of a key-range-split query block leaves its partial result:
+// the unnormalised output O~ = sum_j 2^(s_j - m) v_j and (m, l = sum_j
+// 2^(s_j - m)) over the piece's keys (s in log2 units), for every row and
+// query head, in slot `piece`.
+struct SplitOut {
+    float *o;     // [max_pieces][rows][hq][128] fp32
+    float2 *ml;   // [max_pieces][rows][hq]
+    int64_t rows; // rows of the call (sum of the new lengths)
+    int piece_tiles, max_pieces, piece;
+};
+
 __device__ inline int swz(int row) { return ((row & 3) << 2) ^ ((row >> 2) & 3); }
 
 __device__ inline uint32_t cvt2(float a, float b) {
@@ -118,7 +129,10 @@ __device__ inline void wg_barrier() {
 // NW: waves per work-group.  8 (query blocks of 64 positions; waves w and
 // w+4 share a SIMD) or 4 (blocks of 32 positions, two work-groups per CU):
 // the same per-wave work, for grids that would leave CUs idle with 8.
-template <bool kTableInLds, int NW>
+// kSplit (4 waves only): the work-group computes piece sp.piece of its query
+// block's key range (prefill_pieces), writing partials to sp when the block
+// has more than one piece and the normalised output otherwise.
+template <bool kTableInLds, int NW, bool kSplit = false>
 __device__ __forceinline__ void
 prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpool,
               const uint16_t *__restrict__ q, uint16_t *__restrict__ out,
@@ -128,8 +142,9 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
               // work-group coordinates (x: query block and heads, b: sequence)
               // and the LDS buffers: K and V tiles (2 * TILE each, 1024-byte
               // aligned) and the block-table copy (kBtCache entries)
-              const int x, const int b, uint16_t *s_k, uint16_t *s_v, int32_t *s_bt) {
+              const int x, const int b, uint16_t *s_k, uint16_t *s_v, int32_t *s_bt, const SplitOut sp = {}) {
     static_assert(NW == 8 || NW == 4, "8 or 4 waves");
+    static_assert(!kSplit || NW == 4, "the key-range split runs 4-wave blocks");
     constexpr int kBM = 8 * NW;         // query positions per block
     constexpr int kNT = 64 * NW;        // threads
     constexpr int kRows = 64 / NW;      // tile rows (keys) each wave loads
@@ -148,6 +163,18 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
     if (pair >= (paired ? (nqb + 1) / 2 : nqb)) return;
     const int n_items = (!paired || pair == nqb - 1 - pair) ? 1 : 2;
     const int r = prefix_lens[b];
+    // key tiles [t_lo, t_hi) of this work-group's (single) block and its
+    // number of pieces (1 without the split); tile t_lo is loaded first and
+    // page p of the sequence sits at s_bt[p - 4 t_lo] in the table copy
+    int t_lo = 0, t_hi = 0, n_pieces = 1;
+    if constexpr (kSplit) {
+        const int nt_b = prefill_block_tiles(r, n, nqb - 1 - pair);
+        n_pieces = prefill_pieces(nt_b, sp.piece_tiles, sp.max_pieces);
+        if (sp.piece >= n_pieces) return;
+        t_lo = sp.piece * nt_b / n_pieces;
+        t_hi = (sp.piece + 1) * nt_b / n_pieces;
+    }
+    const int pbase = 4 * t_lo;
     const int32_t *btrow = bt + static_cast<size_t>(b) * bt_stride;
     const int np_seq = min((r + n + kPageSize - 1) / kPageSize, bt_stride);
 
@@ -162,8 +189,8 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
     // block-table entries of this work-group's keys (the heavier block's)
     {
         const int nt_a = (r + min((nqb - pair) * kBM, n) + BN - 1) / BN;
-        const int np_wg = min(4 * nt_a, np_seq);
-        for (int i = threadIdx.x; i < min(np_wg, kBtCache); i += kNT) s_bt[i] = btrow[i];
+        const int np_wg = min(4 * (kSplit ? t_hi : nt_a), np_seq);
+        for (int i = pbase + threadIdx.x; i < min(np_wg, pbase + kBtCache); i += kNT) s_bt[i - pbase] = btrow[i];
     }
     const int seq_len = r + n;
 
@@ -228,9 +255,9 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
         int page = -1;
         if (p < np_seq) {
             if constexpr (kTableInLds)
-                page = __builtin_amdgcn_readfirstlane(s_bt[p]);
+                page = __builtin_amdgcn_readfirstlane(s_bt[p - pbase]);
             else
-                page = p < kBtCache ? __builtin_amdgcn_readfirstlane(s_bt[p]) : btrow[p];
+                page = p - pbase < kBtCache ? __builtin_amdgcn_readfirstlane(s_bt[p - pbase]) : btrow[p];
         }
         return page_ref(p, page);
     };
@@ -355,7 +382,8 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
     // HBM, so the loads can start before the table copy in LDS is complete
     // (its K and, unless the V loads follow one phase later, its V).
     auto first_tile = [&](auto with_v) __attribute__((always_inline)) {
-        const PageRef ref = page_ref(lpage, lpage < np_seq ? btrow[lpage] : -1);
+        const int p0 = pbase + lpage;
+        const PageRef ref = page_ref(p0, p0 < np_seq ? btrow[p0] : -1);
         const __amdgpu_buffer_rsrc_t rk = page_rsrc(kpool, ref), rv = page_rsrc(vpool, ref);
 #pragma unroll
         for (int j = 0; j < kJ; ++j) {
@@ -456,12 +484,13 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
         } else
         // Tile t+1 is loaded (into the other buffer) while tile t is processed;
         // the K and V pages of a tile are the same pages of the pool.
-        for (int t = 0; t < nt; ++t) {
-            const bool more = t + 1 < nt;
+        for (int t = t_lo; t < (kSplit ? t_hi : nt); ++t) {
+            const int u = t - t_lo;  // tile buffer parity
+            const bool more = t + 1 < (kSplit ? t_hi : nt);
             const PageRef ref = more ? tile_page(t + 1) : PageRef{0, 0};
             const __amdgpu_buffer_rsrc_t rk = page_rsrc(kpool, ref), rv = page_rsrc(vpool, ref);
-            uint16_t *dk = s_k + ((t + 1) & 1) * TILE;
-            uint16_t *dv = s_v + ((t + 1) & 1) * TILE;
+            uint16_t *dk = s_k + ((u + 1) & 1) * TILE;
+            uint16_t *dv = s_v + ((u + 1) & 1) * TILE;
             auto load = [&](int j) __attribute__((always_inline)) {
                 if (more) {
                     if (j < kJ)
@@ -471,9 +500,9 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
                 }
             };
             if (active) {
-                mfma_phase(flag<false>(), flag<true>(), t & 1, t & 1, load);
+                mfma_phase(flag<false>(), flag<true>(), u & 1, u & 1, load);
                 softmax_phase(t);
-                mfma_phase(flag<true>(), flag<false>(), t & 1, t & 1, [](int) {});
+                mfma_phase(flag<true>(), flag<false>(), u & 1, u & 1, [](int) {});
             } else {
 #pragma unroll
                 for (int j = 0; j < 2 * kJ; ++j) load(j);
@@ -482,6 +511,39 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
             wg_barrier();
         }
 
+        if constexpr (kSplit) {
+            if (n_pieces > 1) {
+                // ---- this piece's partial: (m, l) and the unnormalised O of
+                // every row, fp32.  The wave's 32 x 128 tile (16 KiB; waves 0-1
+                // in the K buffers, 2-3 in the V buffers) is staged in LDS so
+                // every store writes whole 512-byte rows; row q holds its
+                // 16-byte chunk c (dims 4c..4c+3) at chunk c ^ (q % 32).
+                const float lt = l_run + __shfl_xor(l_run, 32);
+                char *st = reinterpret_cast<char *>(wave < 2 ? s_k : s_v) + (wave & 1) * (32 * 512);
+#pragma unroll
+                for (int db = 0; db < 4; ++db)
+#pragma unroll
+                    for (int i4 = 0; i4 < 4; ++i4) {
+                        const int c = 8 * db + 2 * i4 + g;
+                        *reinterpret_cast<float4 *>(st + l32 * 512 + 16 * (c ^ l32)) =
+                            make_float4(oacc[db][4 * i4 + 0], oacc[db][4 * i4 + 1], oacc[db][4 * i4 + 2],
+                                        oacc[db][4 * i4 + 3]);
+                    }
+                if (active) {
+                    const size_t slot = static_cast<size_t>(sp.piece) * sp.rows + row0;
+#pragma unroll
+                    for (int j = 0; j < 16; ++j) {
+                        const int row = 2 * j + (lane >> 5), c = lane & 31;
+                        const float4 v = *reinterpret_cast<const float4 *>(st + row * 512 + 16 * (c ^ row));
+                        const int prow = qblk * kBM + row;
+                        if (prow < n)
+                            *reinterpret_cast<float4 *>(sp.o + ((slot + prow) * hq + h) * kHeadDim + 4 * c) = v;
+                    }
+                    if (g == 0 && pos < n) sp.ml[(slot + pos) * hq + h] = make_float2(m_run, lt);
+                }
+                continue;
+            }
+        }
         // ---- normalise and write O[pos][h][d].  The wave's 32 x 128 tile is
         // staged in LDS (the K/V buffers are free now) so that every store
         // writes 16 bytes per lane and four whole 256-byte rows per

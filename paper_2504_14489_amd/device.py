@@ -66,6 +66,7 @@ class DeviceWorkload:
         self.o_pre = torch.zeros_like(self.q_pre)
         self.o_dec = torch.zeros_like(self.q_dec)
         self._ws = {}
+        self._pre_ws = None
         self._pre_args = {}
         self._dec_start = None
 
@@ -86,15 +87,34 @@ class DeviceWorkload:
             self._pre_args[key] = (_dev32([0, n], self.device), _dev32([r], self.device))
         return self._pre_args[key]
 
-    def prefill(self, r: int, n: int, stream=0, timing=None, out: Optional[torch.Tensor] = None):
+    def prefill_workspace(self) -> torch.Tensor:
+        """Workspace for the key-range split of any of the workload's prefill
+        chunks on any stream (the split is used only where the launch would
+        leave CUs idle)."""
+        if self._pre_ws is None:
+            nbytes = max([mw.mw_prefill_workspace_size(self.hq, self.hkv, self.d, [n], [r])
+                          for r, n in self.cfg.pre_chunks] + [16])
+            self._pre_ws = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        return self._pre_ws
+
+    def prefill(self, r: int, n: int, stream=0, timing=None, out: Optional[torch.Tensor] = None,
+                split: bool = True):
         """Causal prefill of positions [r, r+n) over prefix r; returns the
-        output rows [n][Hq][D] (a view of ``out`` or of the workload's buffer)."""
+        output rows [n][Hq][D] (a view of ``out`` or of the workload's buffer).
+        split=False: the plain call, without the key-range split."""
         indptr, pref = self._prefill_args(r, n)
         q = self.q_pre[r:r + n]
         o = self.o_pre[r:r + n] if out is None else out
-        mw.mw_prefill_attn(self.pool, self.hq, self.hkv, self.d, self.scale, [n], [r],
-                           indptr.data_ptr(), pref.data_ptr(), self.pre_bt.data_ptr(),
-                           self.pre_bt.shape[1], q.data_ptr(), o.data_ptr(), stream, timing)
+        if split:
+            ws = self.prefill_workspace()
+            mw.mw_prefill_attn_ws(self.pool, self.hq, self.hkv, self.d, self.scale, [n], [r],
+                                  indptr.data_ptr(), pref.data_ptr(), self.pre_bt.data_ptr(),
+                                  self.pre_bt.shape[1], q.data_ptr(), o.data_ptr(), ws.data_ptr(),
+                                  ws.numel(), stream, timing)
+        else:
+            mw.mw_prefill_attn(self.pool, self.hq, self.hkv, self.d, self.scale, [n], [r],
+                               indptr.data_ptr(), pref.data_ptr(), self.pre_bt.data_ptr(),
+                               self.pre_bt.shape[1], q.data_ptr(), o.data_ptr(), stream, timing)
         return o
 
     def write_prefill_kv(self, r: int, n: int, k_new: torch.Tensor, v_new: torch.Tensor,
@@ -189,6 +209,13 @@ class Timing:
 
     def kernel_ms(self, k: int) -> float:
         return mw.mw_timing_kernel_ms(self.h, k)
+
+    def kernels(self) -> int:
+        return mw.mw_timing_kernels(self.h)
+
+    def all_kernels_ms(self) -> float:
+        """GPU time of every kernel of the call (a split prefill has two)."""
+        return sum(self.kernel_ms(k) for k in range(self.kernels()))
 
 
 class Partition:

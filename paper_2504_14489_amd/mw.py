@@ -129,6 +129,10 @@ _SIGNATURES = {
     "mw_timing_offsets": ([_P, _P, _PF, _PF], _I),
     "mw_prefill_attn": ([_P, ctypes.POINTER(_AttnShape), _I, _PI, _PI, _P, _P, _P, _I, _P, _P, _P,
                          _P], _I),
+    "mw_prefill_workspace_size": ([ctypes.POINTER(_AttnShape), _I, _PI, _PI, _I,
+                                   ctypes.POINTER(ctypes.c_size_t)], _I),
+    "mw_prefill_attn_ws": ([_P, ctypes.POINTER(_AttnShape), _I, _PI, _PI, _P, _P, _P, _I, _P, _P, _P,
+                            ctypes.c_size_t, _P, _P], _I),
     "mw_decode_workspace_size": ([ctypes.POINTER(_AttnShape), _I, _PI, _I,
                                   ctypes.POINTER(ctypes.c_size_t)], _I),
     "mw_decode_attn": ([_P, ctypes.POINTER(_AttnShape), _I, _PI, _P, _P, _I, _P, _P, _P,
@@ -372,6 +376,28 @@ def mw_prefill_attn(pool, num_q_heads: int, num_kv_heads: int, head_dim: int, sc
     _check(load().mw_prefill_attn(pool, ctypes.byref(sh), len(nl), _pi(nl), _pi(pl),
                                   _h(d_qo_indptr), _h(d_prefix_lens), _h(d_block_table), bt_stride,
                                   _h(d_q), _h(d_out), _h(stream), timing))
+
+
+def mw_prefill_workspace_size(num_q_heads: int, num_kv_heads: int, head_dim: int, new_lens,
+                              prefix_lens, num_cus: int = 0) -> int:
+    nl, pl = _i32(new_lens), _i32(prefix_lens)
+    sh = _shape(num_q_heads, num_kv_heads, head_dim, 1.0)
+    out = ctypes.c_size_t()
+    _check(load().mw_prefill_workspace_size(ctypes.byref(sh), len(nl), _pi(nl), _pi(pl), num_cus,
+                                            ctypes.byref(out)))
+    return out.value
+
+
+def mw_prefill_attn_ws(pool, num_q_heads: int, num_kv_heads: int, head_dim: int, scale: float,
+                       new_lens, prefix_lens, d_qo_indptr: int, d_prefix_lens: int,
+                       d_block_table: int, bt_stride: int, d_q: int, d_out: int, d_workspace: int,
+                       workspace_bytes: int, stream=0, timing=None):
+    nl, pl = _i32(new_lens), _i32(prefix_lens)
+    sh = _shape(num_q_heads, num_kv_heads, head_dim, scale)
+    _check(load().mw_prefill_attn_ws(pool, ctypes.byref(sh), len(nl), _pi(nl), _pi(pl),
+                                     _h(d_qo_indptr), _h(d_prefix_lens), _h(d_block_table), bt_stride,
+                                     _h(d_q), _h(d_out), _h(d_workspace), workspace_bytes, _h(stream),
+                                     timing))
 
 
 def mw_decode_workspace_size(num_q_heads: int, num_kv_heads: int, head_dim: int, seq_lens,

@@ -102,6 +102,36 @@ def test_decode_workspace_size(lib):
         assert e.value.status == mw.MW_ERR_UNSUPPORTED
 
 
+def test_prefill_workspace_size(lib):
+    """The split's workspace: pieces x rows x q heads x (512 + 8) bytes.  With
+    no CU count it covers the most pieces (8) any stream's plan can take; on a
+    given CU count the plan cuts only launches of 4-wave blocks (their pairs of
+    64-position blocks fewer than the CUs) and never more than that bound."""
+    row_bytes = 128 * 4 + 8
+    # a one-kv-head shard: 8 q heads, 2048 new tokens over 6144 cached (blocks of
+    # 97..128 key tiles): 32 pairs x 2 head groups = 64 < 96 CUs -> 4-wave blocks
+    assert mw.mw_prefill_workspace_size(8, 1, 128, [2048], [6144], 0) == 8 * 2048 * 8 * row_bytes
+    for cus in (96, 128, 256):
+        b = mw.mw_prefill_workspace_size(8, 1, 128, [2048], [6144], cus)
+        assert b % (2048 * 8 * row_bytes) == 0 and 2 <= b // (2048 * 8 * row_bytes) <= 8, (cus, b)
+    # 8-wave launches (enough pairs for every CU) are never cut
+    assert mw.mw_prefill_workspace_size(8, 1, 128, [2048], [6144], 64) == 0
+    assert mw.mw_prefill_workspace_size(64, 8, 128, [2048], [6144], 96) == 0
+    # a varlen batch: rows of both sequences; the longest block decides the pieces
+    assert mw.mw_prefill_workspace_size(8, 2, 128, [100, 33], [0, 4100], 0) == 8 * 133 * 8 * row_bytes
+    # nothing to cut: blocks of at most 4 key tiles
+    assert mw.mw_prefill_workspace_size(8, 2, 128, [200], [0], 0) == 0
+    assert mw.mw_prefill_workspace_size(8, 2, 128, [], [], 0) == 0
+    for args, status in [((8, 3, 128, [5], [0], 0), mw.MW_ERR_INVALID_ARG),
+                         ((8, 2, 64, [5], [0], 0), mw.MW_ERR_UNSUPPORTED),
+                         ((8, 2, 128, [-1], [0], 0), mw.MW_ERR_INVALID_ARG),
+                         ((8, 2, 128, [5], [-3], 0), mw.MW_ERR_INVALID_ARG),
+                         ((8, 2, 128, [5], [0], -1), mw.MW_ERR_INVALID_ARG)]:
+        with pytest.raises(mw.MWError) as e:
+            mw.mw_prefill_workspace_size(*args)
+        assert e.value.status == status
+
+
 def test_attention_calls_reject_bad_arguments_before_launching(lib):
     pool = mw.mw_kv_pool_create(10, 16, 2, 128, FAKE_K, FAKE_V)
     try:

@@ -5,7 +5,8 @@ import torch
 
 import oracle
 from paper_2504_14489_amd import workloads as W
-from paper_2504_14489_amd.device import DeviceWorkload, to_bits
+from paper_2504_14489_amd import mw
+from paper_2504_14489_amd.device import DeviceWorkload, Partition, Timing, to_bits
 from tests.helpers import assert_close, say
 
 pytestmark = pytest.mark.gpu
@@ -126,7 +127,8 @@ def test_prefill_same_result_on_any_cu_count():
     whole rounds of the stream's CUs, and uses 4-wave work-groups on 32-position
     blocks when the 8-wave pairs would not give every CU one (here: paired
     8-wave blocks on 32 CUs, single 4-wave blocks on 64 and on all CUs); every
-    split must give the same bits."""
+    such choice must give the same bits (the plain call: the key-range split,
+    which changes rounding, is tested on its own)."""
     say("prefill split independence (32 / 64 / all CUs)")
     from paper_2504_14489_amd.device import Partition
     cfg = W.custom_config(hq=32, hkv=8, pre_chunks=((0, 512),), dec_batch=1, dec_len_lo=1,
@@ -138,7 +140,7 @@ def test_prefill_same_result_on_any_cu_count():
         for p_cus in (32, 64, 0):  # 32 pairs: paired on 32 CUs, single blocks otherwise
             part = Partition(p_cus, 256 - p_cus) if p_cus else None
             try:
-                o = dw.prefill(0, 512, part.prefill_stream if part else 0)
+                o = dw.prefill(0, 512, part.prefill_stream if part else 0, split=False)
                 torch.cuda.synchronize()
                 outs.append(to_bits(o))
             finally:
@@ -248,8 +250,9 @@ def test_prefill_block_table_longer_than_the_lds_copy():
     """A sequence of more than 4096 pages (65,536 tokens): the work-group's
     copy of its block table in LDS holds the first 4096 entries and the rest
     are read from global memory.  130 new tokens over a 70,001-token prefix
-    with one kv head: 4-wave blocks on the whole GPU, 8-wave paired blocks on
-    8 CUs; every row against the oracle."""
+    with one kv head: 4-wave blocks on the whole GPU (plain, and cut into key
+    ranges by the split, each piece's table copy starting at its first page),
+    8-wave paired blocks on 8 CUs; every row against the oracle."""
     from paper_2504_14489_amd.device import Partition
     r, n = 70001, 130
     say(f"prefill long block table r={r} n={n}")
@@ -261,15 +264,65 @@ def test_prefill_block_table_longer_than_the_lds_copy():
     part = Partition(8, 8)
     outs = []
     try:
-        for stream in (0, part.prefill_stream):
-            o = dw.prefill(r, n, stream)
+        for stream, split in ((0, False), (part.prefill_stream, False), (0, True)):
+            t = Timing()
+            o = dw.prefill(r, n, stream, t.h, split=split)
             torch.cuda.synchronize()
             outs.append(to_bits(o).copy())
+            kernels = mw.mw_timing_kernels(t.h)
+            t.close()
     finally:
         part.close()
         dw.close()
+    assert kernels == 2, "the whole-GPU call with a workspace did not split"
     ref = oracle.prefill(wl.q_pre[r:r + n], wl.k_pool, wl.v_pool, wl.pre_bt, r)
-    for o, where in zip(outs, ("whole GPU", "8 CUs")):
+    for o, where in zip(outs, ("whole GPU", "8 CUs", "whole GPU, key-range split")):
         mx, mean = assert_close(o, ref, f"long table on {where}")
         say(f"  {where}: max-abs {mx:.3g} mean-abs {mean:.3g}")
     assert np.array_equal(outs[0], outs[1]), "4-wave and 8-wave launches differ"
+
+
+# (prefix r, new n, q heads, kv heads, CUs of the stream (0: all), the plan
+# must cut): causal blocks long enough to be cut into key ranges, ragged
+# tails, a GQA group of 6 (idle waves in the second head group), a
+# one-kv-head shard of a 70B-shaped layer (2048-token chunks: the first on the
+# whole GPU, the last on 96 CUs), and calls the plan may keep whole (short
+# blocks on 96 CUs, a grid of two blocks per CU, one 5-tile block)
+SPLIT_CASES = [(1000, 130, 8, 2, 0, True), (333, 257, 12, 2, 0, True), (0, 2048, 8, 1, 0, True),
+               (6144, 2048, 8, 1, 96, True), (4100, 33, 4, 1, 0, True), (0, 1000, 8, 2, 0, True),
+               (0, 2048, 8, 1, 96, False), (0, 1000, 32, 8, 0, False), (257, 1, 8, 1, 0, False)]
+
+
+@pytest.mark.parametrize("r,n,hq,hkv,cus,must_cut", SPLIT_CASES)
+def test_prefill_key_range_split(r, n, hq, hkv, cus, must_cut):
+    """Prefill with the key-range split (pieces of each causal block's keys,
+    merged by log-sum-exp) against the oracle on every row.  The call splits
+    exactly when the workspace size for the stream's CU count says the plan
+    cuts, and the result is the same from run to run."""
+    say(f"prefill key-range split r={r} n={n} hq={hq} hkv={hkv} cus={cus or 'all'}")
+    cfg = W.custom_config(hq=hq, hkv=hkv, pre_chunks=((r, n),), dec_batch=1, dec_len_lo=1, dec_len_hi=2,
+                          seed=r + 3 * n)
+    wl = W.make_workload(cfg)
+    dw = DeviceWorkload(wl)
+    part = Partition(cus, 256 - cus) if cus else None
+    stream = part.prefill_stream if part else 0
+    outs, kernels = [], []
+    try:
+        for _ in range(2):
+            t = Timing()
+            o = dw.prefill(r, n, stream, t.h)
+            torch.cuda.synchronize()
+            outs.append(to_bits(o).copy())
+            kernels.append(mw.mw_timing_kernels(t.h))
+            t.close()
+    finally:
+        if part:
+            part.close()
+        dw.close()
+    assert np.array_equal(outs[0], outs[1]), "run-to-run results differ"
+    planned = mw.mw_prefill_workspace_size(hq, hkv, 128, [n], [r], cus or 256) > 0
+    assert planned or not must_cut, "the plan does not cut"
+    assert (kernels[0] == 2) == planned, f"{kernels[0]} kernel(s), plan cuts: {planned}"
+    ref = oracle.prefill(wl.q_pre[r:r + n], wl.k_pool, wl.v_pool, wl.pre_bt, r)
+    mx, mean = assert_close(outs[0], ref, f"split r={r} n={n}")
+    say(f"  {kernels[0]} kernel(s): max-abs {mx:.3g} mean-abs {mean:.3g}")
