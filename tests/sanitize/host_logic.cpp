@@ -79,8 +79,26 @@ void planners() {
                           reinterpret_cast<int32_t *>(g_fake), reinterpret_cast<int32_t *>(g_fake), pstride,
                           g_fake, g_fake};
         mw::PrefillPlan pp;
-        if (mw::prefill_prepare(&p, 8 * uniform(1, 32), uniform(0, 1), &pp, "prefill_prepare") == MW_OK)
+        const int pcus = 8 * uniform(1, 32);
+        if (mw::prefill_prepare(&p, pcus, uniform(0, 1), &pp, "prefill_prepare") == MW_OK) {
             check(pp.gx >= 0 && (pp.waves == 4 || pp.waves == 8) && pp.group == group, "prefill plan", it);
+            // the key-range split: at most the pieces the size call with no CU
+            // count allows, pieces of at least 4 tiles, never cut 8-wave launches
+            mw::prefill_split_plan(pb, nl.data(), pl.data(), shape.num_q_heads, pcus, &pp);
+            size_t most = 0;
+            check(mw_prefill_workspace_size(&shape, pb, nl.data(), pl.data(), 0, &most) == MW_OK, "size call", it);
+            check(pp.split_bytes <= most, "the size with no CU count covers the plan", it);
+            check(pp.pieces >= 1 && pp.pieces <= mw::kPrefillMaxPieces, "pieces", it);
+            check(pp.pieces == 1 || (pp.waves == 4 && pp.piece_tiles >= mw::kPrefillMinPieceTiles), "cuts", it);
+            for (int b = 0; b < pb; ++b)
+                for (int qb = 0; 32 * qb < nl[b] && pp.pieces > 1; ++qb) {
+                    const int nt = mw::prefill_block_tiles(pl[b], nl[b], qb);
+                    const int k = mw::prefill_pieces(nt, pp.piece_tiles, pp.pieces);
+                    // the last cut leaves the block's last two tiles (its diagonal) in the last piece
+                    check(k == 1 || (k - 1) * nt / k <= nt - 2, "cut before the diagonal", it);
+                    check(k == 1 || (k - 1) * nt / k <= (pl[b] + 32 * qb) / 64, "first tile of each piece visible", it);
+                }
+        }
         mw_kv_pool_destroy(pool);
     }
 }
