@@ -477,6 +477,8 @@ typedef struct {
     int32_t bt_stride;
     const void *d_q;
     void *d_out;
+    void *d_workspace;      /* NULL: the plain call (mw_prefill_attn); else the */
+    size_t workspace_bytes; /* key-range split's workspace (mw_prefill_attn_ws) */
 } mw_prefill_args;
 typedef struct {
     int32_t config;             /* partition index, 0 <= config < n */

@@ -314,6 +314,10 @@ mw_status mw_engine_run(mw_engine *eng, const mw_decode_args *dec, const mw_pref
                               dec->workspace_bytes, dec->chunk_pages, s, nullptr);
     };
     auto prefill_call = [&](hipStream_t s) {
+        if (pre->d_workspace)
+            return mw_prefill_attn_ws(pre->pool, &pre->shape, pre->batch, pre->h_new_lens, pre->h_prefix_lens,
+                                      pre->d_qo_indptr, pre->d_prefix_lens, pre->d_block_table, pre->bt_stride,
+                                      pre->d_q, pre->d_out, pre->d_workspace, pre->workspace_bytes, s, nullptr);
         return mw_prefill_attn(pre->pool, &pre->shape, pre->batch, pre->h_new_lens, pre->h_prefix_lens,
                                pre->d_qo_indptr, pre->d_prefix_lens, pre->d_block_table, pre->bt_stride, pre->d_q,
                                pre->d_out, s, nullptr);

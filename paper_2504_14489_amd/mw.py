@@ -66,7 +66,8 @@ class _PrefillArgs(ctypes.Structure):
                 ("h_new_lens", ctypes.c_void_p), ("h_prefix_lens", ctypes.c_void_p),
                 ("d_qo_indptr", ctypes.c_void_p), ("d_prefix_lens", ctypes.c_void_p),
                 ("d_block_table", ctypes.c_void_p), ("bt_stride", ctypes.c_int32),
-                ("d_q", ctypes.c_void_p), ("d_out", ctypes.c_void_p)]
+                ("d_q", ctypes.c_void_p), ("d_out", ctypes.c_void_p),
+                ("d_workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t)]
 
 
 class EnginePlan(ctypes.Structure):
@@ -546,7 +547,8 @@ def _engine_structs(dec: dict, pre: dict):
                      dec.get("chunk_pages", 0))
     pa = _PrefillArgs(_h(pre["pool"]), _shape(pre["hq"], pre["hkv"], pre["head_dim"], pre["scale"]), len(nl),
                       nl.ctypes.data, pl.ctypes.data, _h(pre["d_qo_indptr"]), _h(pre["d_prefix_lens"]),
-                      _h(pre["d_block_table"]), pre["bt_stride"], _h(pre["d_q"]), _h(pre["d_out"]))
+                      _h(pre["d_block_table"]), pre["bt_stride"], _h(pre["d_q"]), _h(pre["d_out"]),
+                      _h(pre.get("d_workspace")), pre.get("workspace_bytes", 0))
     return da, pa, (sl, nl, pl)
 
 

@@ -70,18 +70,24 @@ class Pool:
 
 
 class PrefillCall:
-    def __init__(self, pool: Pool, n: int, r: int):
+    """One prefill call on a stream of `cus` CUs, with the key-range split's
+    workspace when its plan cuts (calls whose few query blocks would leave
+    CUs idle then spread over all of them)."""
+
+    def __init__(self, pool: Pool, n: int, r: int, cus: int):
         self.p, self.n, self.r = pool, n, r
         self.bt, self.stride = pool.tables([r + n])
         self.q = pool.rand(n, HQ, D)
         self.o = torch.empty_like(self.q)
         self.indptr = torch.tensor([0, n], dtype=torch.int32, device=pool.dev)
         self.pref = torch.tensor([r], dtype=torch.int32, device=pool.dev)
+        nbytes = mw.mw_prefill_workspace_size(HQ, HKV, D, [n], [r], cus)
+        self.ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=pool.dev)
 
     def __call__(self, stream, timing=None):
-        mw.mw_prefill_attn(self.p.pool, HQ, HKV, D, self.p.scale, [self.n], [self.r], self.indptr.data_ptr(),
-                           self.pref.data_ptr(), self.bt.data_ptr(), self.stride, self.q.data_ptr(),
-                           self.o.data_ptr(), stream, timing)
+        mw.mw_prefill_attn_ws(self.p.pool, HQ, HKV, D, self.p.scale, [self.n], [self.r], self.indptr.data_ptr(),
+                              self.pref.data_ptr(), self.bt.data_ptr(), self.stride, self.q.data_ptr(),
+                              self.o.data_ptr(), self.ws.data_ptr(), self.ws.numel(), stream, timing)
 
 
 class DecodeCall:
@@ -107,7 +113,7 @@ def solo_ms(call, stream, reps: int, kernel_only: bool) -> float:
     for t in ts:
         call(stream, t.h)
     torch.cuda.synchronize()
-    vals = [t.kernel_ms(0) if kernel_only else t.elapsed()[0] for t in ts[1:]]
+    vals = [t.all_kernels_ms() if kernel_only else t.elapsed()[0] for t in ts[1:]]
     for t in ts:
         t.close()
     return statistics.median(vals)
@@ -303,7 +309,7 @@ def main(argv=None):
                              int(rng.integers(0, grid_r[-1] + 1)), False) for _ in range(args.held_out)]
                 pre_calls = {}
                 for n, r, grid in pre_pts:
-                    c = PrefillCall(pool, n, r)
+                    c = PrefillCall(pool, n, r, pc)
                     ms = solo_ms(c, part.prefill_stream, args.reps, kernel_only=True)
                     result["prefill"].append({"cus": pc, "n": n, "r": r, "ms": ms, "grid": grid})
                     if grid and n in guard_n and r in guard_r:
