@@ -193,3 +193,43 @@ def test_graph_launched_on_a_partition_stream_keeps_its_cus():
         del g
     finally:
         part.close()
+
+
+def test_engine_prefill_with_split_workspace():
+    """Prefill arguments that carry a workspace make the engine issue
+    key-range-split calls: a short chunk over a long prefix with one kv head
+    has too few query blocks for a 64-CU partition, so the call is cut; the
+    engine's outputs equal one split call on that partition's stream, and
+    the oracle's."""
+    from paper_2504_14489_amd.device import Timing
+    cfg = W.custom_config("engine_split", hq=8, hkv=1, pre_chunks=((2000, 64),), dec_batch=3,
+                          dec_len_lo=100, dec_len_hi=400)
+    wl = W.make_workload(cfg, seed=12)
+    dw = DeviceWorkload(wl)
+    eng = Engine([64])
+    try:
+        dec, pre = dw.engine_args()
+        nbytes = mw.mw_prefill_workspace_size(dw.hq, dw.hkv, dw.d, pre["new_lens"], pre["prefix_lens"], 64)
+        assert nbytes > 0, "the plan does not cut on 64 CUs"
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=dw.device)
+        pre = dict(pre, d_workspace=ws.data_ptr(), workspace_bytes=ws.numel())
+        say("engine run with a split prefill workspace")
+        ps, ds = eng.streams(0)
+        t = Timing()
+        mw.mw_prefill_attn_ws(pre["pool"], dw.hq, dw.hkv, dw.d, dw.scale, pre["new_lens"], pre["prefix_lens"],
+                              pre["d_qo_indptr"], pre["d_prefix_lens"], pre["d_block_table"], pre["bt_stride"],
+                              pre["d_q"], pre["d_out"], ws.data_ptr(), ws.numel(), ps, t.h)
+        mw.mw_sync(ps)
+        assert t.kernels() == 2, "the plain split call did not cut"
+        ref_pre = dw.o_pre.clone()
+        dw.o_pre.zero_()
+        torch.cuda.synchronize()
+        eng.run(dec, pre, config=0, decode_iters=2, decode_layers=2, prefill_layers=6, layers_per_launch=2,
+                policy=mw.MW_ENGINE_POLLED, switch_on_decode_end=False)
+        assert torch.equal(dw.o_pre, ref_pre), "engine prefill differs from the split call"
+        c = wl.cfg
+        ref = oracle.prefill(wl.q_pre[2000:2064], wl.k_pool, wl.v_pool, wl.pre_bt, 2000)
+        assert_close(to_bits(dw.o_pre[2000:2064]), ref, "engine split prefill")
+    finally:
+        eng.close()
+        dw.close()
