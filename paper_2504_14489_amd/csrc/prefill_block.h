@@ -380,7 +380,8 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
 
     // The first tile of an item: its pages straight from the block table in
     // HBM, so the loads can start before the table copy in LDS is complete
-    // (its K and, unless the V loads follow one phase later, its V).
+    // (its K and, with 4 waves, its V; the 8-wave body loads V(0) in its
+    // first period).
     auto first_tile = [&](auto with_v) __attribute__((always_inline)) {
         const int p0 = pbase + lpage;
         const PageRef ref = page_ref(p0, p0 < np_seq ? btrow[p0] : -1);
@@ -390,7 +391,6 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
             page_load(rk, s_k, j);
             if constexpr (decltype(with_v)::value) page_load(rv, s_v, j);
         }
-        return ref;
     };
 
     for (int item = 0; item < n_items; ++item) {
@@ -400,7 +400,7 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
         qabs = r + pos;
         diag = r + qblk * kBM + (wave >> 2) * 32;  // smallest query of the wave
         if (item > 0) wg_barrier();  // the previous item's output staging is done
-        PageRef ref_t = first_tile(flag<NW == 4>());
+        first_tile(flag<NW == 4>());
         // Q^T operand, all 8 dim-steps (k = 16*kb + 8*g + e)
         {
             const bool ok = active && pos < n;
@@ -435,39 +435,72 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
             const int grp = wave >> 2;
             // Each wave runs its own sequence M(0) S(0) M(1) .. S(nt-1) M(nt),
             // group 1 one phase after group 0 (a barrier ends every phase, 2nt+2
-            // in all for both groups).  The loads of period t go out at its
-            // first phase (group 0: before M(t); group 1: before S(t-1)) and
-            // are waited for at its last (group 0: after S(t); group 1: after
-            // M(t)).
-            auto period_loads = [&](int t) __attribute__((always_inline)) {
-                const PageRef ref_n = t + 1 < nt ? tile_page(t + 1) : PageRef{0, 0};
-                if (t + 1 < nt) {
-                    const __amdgpu_buffer_rsrc_t rk = page_rsrc(kpool, ref_n);
+            // in all for both groups).  Group 1 issues all loads of period t
+            // (K(t+1) and V(t), one page of each per wave) at the start of
+            // phase 2t, its softmax phase, and waits for them at the end of
+            // phase 2t+1: group 0's matrix phases issue only MFMAs and their
+            // operand reads.
+            const int lw = wave & 3;  // page of the tile a group-1 wave loads
+            int goffp[4];
 #pragma unroll
-                    for (int j = 0; j < kJ; ++j) page_load(rk, s_k + ((t + 1) & 1) * TILE, j);
+            for (int j = 0; j < 4; ++j) {
+                const int row = 4 * j + (lane >> 4);
+                goffp[j] = 2 * (row * kHeadDim + 8 * ((lane & 15) ^ swz(row)));
+            }
+            auto page_load_full = [&](__amdgpu_buffer_rsrc_t rsrc, uint16_t *dst, int j) __attribute__((always_inline)) {
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rsrc, reinterpret_cast<lds_void *>(reinterpret_cast<uintptr_t>(dst + (16 * lw + 4 * j) * ROW)),
+                    16, goffp[j], 0, 0, 0);
+            };
+            // Block-table entry of page lw of tile it.  With the whole table in
+            // LDS it is read one period before its loads (pg_n), so they never
+            // wait for an LDS read, and taken as read (entry 0 past the
+            // sequence): page_ref gives pages past the sequence no bytes and
+            // tiles past the block are not loaded, so no select waits for it.
+            auto table_entry = [&](int it) __attribute__((always_inline)) {
+                const int p = 4 * it + lw;
+                const bool ok = it < nt && p < np_seq;
+                if constexpr (kTableInLds)
+                    return s_bt[ok ? p - pbase : 0];
+                else
+                    return ok ? (p - pbase < kBtCache ? s_bt[p - pbase] : btrow[p]) : -1;
+            };
+            int pg_n = 0;
+            PageRef ref_v{0, 0};  // page lw of tile t, whose V is loaded in period t
+            auto period_loads = [&](int t) __attribute__((always_inline)) {
+                PageRef ref_k;
+                if constexpr (kTableInLds) {
+                    ref_k = page_ref(4 * (t + 1) + lw, __builtin_amdgcn_readfirstlane(pg_n));
+                    pg_n = table_entry(t + 2);
+                } else {
+                    ref_k = page_ref(4 * (t + 1) + lw, __builtin_amdgcn_readfirstlane(table_entry(t + 1)));
+                }
+                if (t + 1 < nt) {
+                    const __amdgpu_buffer_rsrc_t rk = page_rsrc(kpool, ref_k);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) page_load_full(rk, s_k + ((t + 1) & 1) * TILE, j);
                 }
                 if (t < nt) {
-                    const __amdgpu_buffer_rsrc_t rv = page_rsrc(vpool, ref_t);
+                    const __amdgpu_buffer_rsrc_t rv = page_rsrc(vpool, ref_v);
 #pragma unroll
-                    for (int j = 0; j < kJ; ++j) page_load(rv, s_v + (t & 1) * TILE, j);
+                    for (int j = 0; j < 4; ++j) page_load_full(rv, s_v + (t & 1) * TILE, j);
                 }
-                ref_t = ref_n;
+                ref_v = ref_k;
             };
             auto vm_wait = [&]() __attribute__((always_inline)) { __builtin_amdgcn_s_waitcnt(0x0F70); };
-            if (grp == 1) {  // group 1's first phase: none of its own work
+            if (grp == 1) {  // group 1's first phase: the loads of period 0
+                ref_v = page_ref(lw, __builtin_amdgcn_readfirstlane(table_entry(0)));
+                if constexpr (kTableInLds) pg_n = table_entry(1);
                 period_loads(0);
                 wg_barrier();
             }
-            if (grp == 0) period_loads(0);
             if (active) mfma_phase(flag<false>(), flag<true>(), 0, 0, [](int) {});  // M(0): S(0) = K(0) Q^T
             if (grp == 1) vm_wait();
             wg_barrier();
             for (int t = 0; t + 1 < nt; ++t) {
                 if (grp == 1) period_loads(t + 1);
                 if (active) softmax_phase(t);
-                if (grp == 0) vm_wait();
                 wg_barrier();
-                if (grp == 0) period_loads(t + 1);
                 if (active)  // M(t+1): O += V(t)^T P(t)^T, S(t+1) = K(t+1) Q^T
                     mfma_phase(flag<true>(), flag<true>(), (t + 1) & 1, t & 1, [](int) {});
                 if (grp == 1) vm_wait();
@@ -475,10 +508,8 @@ prefill_block(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ v
             }
             // the last tile: softmax(nt-1), then M(nt) = O += V(nt-1)^T P(nt-1)^T
             if (active) softmax_phase(nt - 1);
-            if (grp == 0) vm_wait();
             wg_barrier();
             if (active) mfma_phase(flag<true>(), flag<false>(), 0, (nt - 1) & 1, [](int) {});
-            if (grp == 1) vm_wait();
             wg_barrier();
             if (grp == 0) wg_barrier();  // group 0's last phase: none of its own work
         } else
