@@ -9,9 +9,10 @@ first, as the paper launches the decode iteration before prefill, Sec. 3.2.2):
                   = split kernel + combine kernel)
   prefill stream: append each chunk's new K/V, causal prefill attention
 
-m is the number of decode iterations that fit in one prefill call on the
-isolated partitions (at least 1), so both partitions stay busy for the whole
-timed region, as in the paper's bubble-less multiplexing.
+m is the number of decode iterations that fit in one prefill call when the
+two run side by side (at least 1; from the warm-up of the multiplexed loop),
+so both partitions stay busy for the whole timed region, as in the paper's
+bubble-less multiplexing.
 
 The default run measures every workload in turn (tiny as a parity case, the
 8B- and 70B-shaped layers, one GPU's tensor-parallel-8 shard of the 70B layer,
@@ -421,9 +422,18 @@ def run_partition(b, p_cus, d_cus, p_index, args):
         tp = median(iso_p["call"])
         td = median(iso_d["call"])
         m = max(1, int(round(tp / td)))
-        log(f"[bench] {b.cfg.name} {p_cus}/{d_cus}: isolated prefill {tp:.3f} ms, decode {td:.3f} ms "
-            f"-> {m} decode iteration(s) per step")
-        b.multiplexed(part, max(1, args.warmup), m)     # warm-up of the multiplexed loop
+        # warm-up of the multiplexed loop; the decode iterations per step are
+        # then taken from its multiplexed times, so that the decode stream stays
+        # busy for the whole prefill window (isolated times understate the
+        # prefill's slowdown and would leave the last prefill launches alone)
+        warm = b.multiplexed(part, max(2, args.warmup), m)
+        m_mux = max(1, int(round(median(warm["prefill_k"]) / median(warm["decode_call"]))))
+        log(f"[bench] {b.cfg.name} {p_cus}/{d_cus}: isolated prefill {tp:.3f} ms, decode {td:.3f} ms; "
+            f"multiplexed {median(warm['prefill_k']):.3f} / {median(warm['decode_call']):.3f} ms "
+            f"-> {m_mux} decode iteration(s) per step")
+        if m_mux != m:
+            m = m_mux
+            b.multiplexed(part, max(1, args.warmup), m)
         b.dw.o_pre.zero_()
         b.dw.o_dec.zero_()
         mux = b.multiplexed(part, args.steps, m, MARK_BASE + 64 * b.index + 2 * p_index)
