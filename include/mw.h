@@ -354,10 +354,33 @@ mw_status mw_decode_attn_noalloc(const mw_kv_pool *pool, const mw_attn_shape *sh
  *   mw_predictor_*_ms: the model's prediction; MW_ERR_NOT_READY if no model
  *       was fitted for that phase and partition size.
  *   mw_predictor_coefficients: th1..th4 (prefill) or th1..th3 (decode, th[3]
- *       set to 0) of a fitted model.  phase: 0 = prefill, 1 = decode. */
+ *       set to 0) of a fitted model.  phase: 0 = prefill (its 8-wave path
+ *       once a launch shape is set), 1 = decode, 2 = prefill on the 4-wave
+ *       path (launch shape set).
+ *
+ *   mw_predictor_set_launch_shape: tells the predictor the attention shape
+ *       of the calls it models (query and kv heads; num_q_heads a multiple of
+ *       num_kv_heads), before any prefill sample is added (else
+ *       MW_ERR_INVALID_ARG).  A single attention call, unlike the paper's
+ *       whole-model iterations, keeps the steps of its launch: rounds of
+ *       work-groups over the partition's CUs, and calls whose few work-groups
+ *       run at once, bound by the longest.  With the shape, each prefill
+ *       call's launch on `cus` CUs is planned as mw_prefill_attn_ws plans it
+ *       (key-range split included) and simulated: the work-groups in dispatch
+ *       order, each to the CU slot that frees first, a work-group's work its
+ *       key tiles.  The n^2, n r and n terms of Eq. (1) are multiplied by the
+ *       load-imbalance factor (the latest CU's time over the time of the same
+ *       work spread evenly), and the kernel path (8-wave or 4-wave blocks)
+ *       selects one of two models per partition size, fitted separately, as
+ *       the paper keeps separate models for separate kernels.  Predicting
+ *       with a path whose model is not fitted uses the other path's model;
+ *       mw_predictor_fit leaves a 4-wave-path model whose samples do not
+ *       determine it unfitted instead of failing.
+ *       Decode keeps Eq. (2) as is. */
 typedef struct mw_predictor mw_predictor;
 mw_status mw_predictor_create(mw_predictor **out);
 mw_status mw_predictor_destroy(mw_predictor *p);
+mw_status mw_predictor_set_launch_shape(mw_predictor *p, int32_t num_q_heads, int32_t num_kv_heads);
 mw_status mw_predictor_add_prefill(mw_predictor *p, int32_t cus, int32_t batch, const int32_t *new_lens,
                                    const int32_t *prefix_lens, double ms);
 mw_status mw_predictor_add_decode(mw_predictor *p, int32_t cus, int32_t batch, const int32_t *seq_lens,

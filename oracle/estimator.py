@@ -11,7 +11,10 @@ Plain numpy, written from the paper's Sec. 3.3 and Sec. 3.4:
   partition size) the maximum decode slowdown observed; token counts in
   powers-of-4 cells, batch sizes in powers-of-2 cells;
 * the number of prefill layers launched next to a decode iteration,
-  N_PL = ceil(T_d * N_T / T_P) (Sec. 3.4), clamped to [1, N_T].
+  N_PL = ceil(T_d * N_T / T_P) (Sec. 3.4), clamped to [1, N_T];
+* the launch-imbalance factor that scales Eq. (1)'s terms for a single
+  attention call (not from the paper: it restates the library's documented
+  prefill launch rules and simulates the dispatch of the work-groups).
 """
 from __future__ import annotations
 
@@ -83,3 +86,105 @@ def guard_lookup(cells: Dict[Tuple, float], key) -> float:
 
 def prefill_layers(t_decode_ms: float, t_prefill_ms: float, n_layers: int) -> int:
     return int(min(max(math.ceil(t_decode_ms * n_layers / t_prefill_ms), 1), n_layers))
+
+
+def prefill_launch(new_lens, prefix_lens, hkv: int, group: int, cus: int) -> Tuple[int, float]:
+    """Kernel path (0: 8-wave, 1: 4-wave) and load-imbalance factor of a prefill
+    call on `cus` CUs, as the library launches it with a split workspace.
+
+    Launch rules: heads = hkv * ceil(group / 4); 64-position query blocks, one
+    work-group per CU, unless their pairs (ceil(ceil(n/64) / 2) per sequence,
+    times heads) number fewer than the CUs: then 32-position blocks, two per
+    CU.  Blocks are paired (block nqb-1-i with block i) when the pairs fill
+    whole rounds of the slots (pairs >= slots and rounds * slots * 20 <=
+    pairs * 21); otherwise single blocks, heaviest first.  With 32-position
+    blocks, the key-range split: units = sum ceil(n/32) * heads, max_nt = key
+    tiles of the heaviest block; k = min(8, max(2, ceil(2 cus / units))) if
+    units < cus, else 3 if units < 2 cus and max_nt >= 96, else no split;
+    pieces of pt = max(4, ceil(max_nt / k)) tiles, at most 8 per block (a block
+    of nt tiles has min(8, ceil(nt / pt)) pieces, piece p covering tiles
+    [p nt / np, (p+1) nt / np)).  Block q of a sequence (n, r) reads
+    ceil((r + min(q bm + bm, n)) / 64) key tiles.
+
+    Dispatch: grid x fastest, then the sequence; grid x enumerates pairs (or
+    blocks) times heads (times pieces, piece fastest, for the split); each
+    work-group goes to the free slot with the earliest free time (ties: the
+    lower slot index on its CU, then the lower CU), and occupies it for its
+    work in tiles.  A CU that holds one work-group of a two-per-CU launch takes
+    its work / 0.9.  Factor = max CU time * cus / total work."""
+    ng = (group + 3) // 4
+    heads = hkv * ng
+    lens = list(zip([int(n) for n in new_lens], [int(r) for r in prefix_lens]))
+    max_n = max(n for n, _ in lens)
+
+    def n_pairs(bm):
+        return sum(((n + bm - 1) // bm + 1) // 2 for n, _ in lens) * heads
+
+    if n_pairs(64) < cus:
+        path, bm, per_cu = 1, 32, 2
+    else:
+        path, bm, per_cu = 0, 64, 1
+    slots = per_cu * cus
+    npairs = n_pairs(bm)
+    rounds = (npairs + slots - 1) // slots
+    paired = npairs >= slots and rounds * slots * 20 <= npairs * 21
+    max_qb = (max_n + bm - 1) // bm
+    pieces, pt = 1, 0
+    if path == 1:
+        units = sum((n + 31) // 32 for n, _ in lens) * heads
+        max_nt = max((r + n + 63) // 64 for n, r in lens if n > 0)
+        k = 1
+        if units < cus:
+            k = min(8, max(2, (2 * cus + units - 1) // units))
+        elif units < 2 * cus and max_nt >= 96:
+            k = 3
+        if k > 1:
+            pt = max(4, (max_nt + k - 1) // k)
+            pieces = min(8, max(1, (max_nt + pt - 1) // pt))
+    work = []
+    for n, r in lens:
+        nqb = (n + bm - 1) // bm
+
+        def tiles(q):
+            return (r + min(q * bm + bm, n) + 63) // 64
+
+        if pieces > 1:
+            for x in range(max_qb * heads * pieces):
+                unit, piece = divmod(x, pieces)
+                pair = unit // heads
+                if pair >= nqb:
+                    continue
+                nt = tiles(nqb - 1 - pair)
+                np_ = min(pieces, max(1, (nt + pt - 1) // pt))
+                if piece < np_:
+                    work.append((piece + 1) * nt // np_ - piece * nt // np_)
+        else:
+            gx = ((max_qb + 1) // 2 if paired else max_qb) * heads
+            for x in range(gx):
+                pair = x // heads
+                last = nqb - 1 - pair
+                if pair >= ((nqb + 1) // 2 if paired else nqb):
+                    continue
+                work.append(tiles(last) + (tiles(pair) if paired and pair != last else 0))
+    total = float(sum(work))
+    if total <= 0:
+        return path, 1.0
+    free = [[0.0, k, c] for k in range(per_cu) for c in range(cus)]
+    load = [0.0] * cus
+    count = [0] * cus
+    for w in work:
+        s = min(free, key=lambda e: (e[0], e[1], e[2]))
+        load[s[2]] += w
+        count[s[2]] += 1
+        s[0] += w
+    t_max = max(load[c] / (0.9 if per_cu == 2 and count[c] == 1 else 1.0) for c in range(cus))
+    return path, t_max * cus / total
+
+
+def prefill_features_launch(new_lens, prefix_lens, hkv: int, group: int, cus: int) -> Tuple[int, np.ndarray]:
+    """Model index (0: 8-wave path, 2: 4-wave path) and Eq. (1) terms with the
+    n^2, n r and n terms multiplied by the launch-imbalance factor."""
+    path, kappa = prefill_launch(new_lens, prefix_lens, hkv, group, cus)
+    x = prefill_features(new_lens, prefix_lens)
+    x[:3] *= kappa
+    return (0 if path == 0 else 2), x

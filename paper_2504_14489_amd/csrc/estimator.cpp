@@ -5,6 +5,7 @@
 #include <algorithm>
 #include <cmath>
 #include <map>
+#include <queue>
 #include <tuple>
 #include <vector>
 
@@ -116,6 +117,80 @@ bool decode_terms(int32_t batch, const int32_t *lens, double out[4]) {
     return true;
 }
 
+// The library's prefill launch on `cus` CUs, from the lengths: its kernel path
+// (0: 8-wave blocks of 64 positions, one work-group per CU; 1: 4-wave blocks
+// of 32 positions, two work-groups per CU, with the key-range split when its
+// plan cuts, as a call with a workspace makes it) and its load-imbalance
+// factor: the latest CU's finishing time over the time of the same work spread
+// evenly over the CUs.  The work-groups are taken in dispatch order (grid x
+// fastest, then the sequence) and each goes to the CU slot that frees first,
+// all CUs' first slots before any second one; a work-group's work is its key
+// tiles (64 keys each), summed over the blocks it takes.  A CU that holds a
+// single work-group of a two-per-CU launch runs it at 0.9 of a shared CU's
+// rate: two work-groups sharing a CU each run about 1.8 times slower than one
+// alone (measured), i.e. the pair moves 2 / 1.8 times the work.
+struct PrefillLaunch {
+    int path;
+    double kappa;
+};
+
+PrefillLaunch prefill_launch(int32_t batch, const int32_t *nl, const int32_t *rl, int hkv, int group, int64_t cus) {
+    PrefillPlan pl;
+    prefill_plan_lengths(batch, nl, hkv, group, cus, true, &pl);
+    if (pl.waves == 4) prefill_split_plan(batch, nl, rl, hkv * group, cus, &pl);
+    const int bm = pl.waves == 4 ? 32 : 64;
+    const int per_cu = pl.waves == 4 ? 2 : 1;
+    const int64_t heads = static_cast<int64_t>(pl.hkv) * pl.n_hgroups;
+    int64_t max_n = 0;
+    for (int32_t b = 0; b < batch; ++b) max_n = std::max<int64_t>(max_n, nl[b]);
+    std::vector<double> work;
+    for (int32_t b = 0; b < batch; ++b) {
+        const int n = nl[b], r = rl[b];
+        const int nqb = (n + bm - 1) / bm;
+        auto tiles = [&](int q) { return (r + std::min(q * bm + bm, n) + 63) / 64; };
+        if (pl.pieces > 1) {  // split kernel: x = unit * pieces + piece, single blocks
+            const int64_t gx = (max_n + bm - 1) / bm * heads * pl.pieces;
+            for (int64_t x = 0; x < gx; ++x) {
+                const int64_t pair = x / pl.pieces / heads;
+                const int piece = static_cast<int>(x % pl.pieces);
+                if (pair >= nqb) continue;
+                const int ntb = tiles(nqb - 1 - static_cast<int>(pair));
+                const int np = prefill_pieces(ntb, pl.piece_tiles, pl.pieces);
+                if (piece >= np) continue;
+                work.push_back((piece + 1) * ntb / np - piece * ntb / np);
+            }
+        } else {
+            for (int64_t x = 0; x < pl.gx; ++x) {
+                const int pair = static_cast<int>(x / heads);
+                const int last = nqb - 1 - pair;
+                if (pl.paired ? pair >= (nqb + 1) / 2 : pair >= nqb) continue;
+                work.push_back(tiles(last) + (pl.paired && pair != last ? tiles(pair) : 0));
+            }
+        }
+    }
+    double total = 0;
+    for (double w : work) total += w;
+    if (!(total > 0)) return {pl.waves == 4 ? 1 : 0, 1.0};
+    using Slot = std::tuple<double, int, int64_t>;  // free time, slot index on its CU, CU
+    std::priority_queue<Slot, std::vector<Slot>, std::greater<Slot>> free_slots;
+    for (int k = 0; k < per_cu; ++k)
+        for (int64_t c = 0; c < cus; ++c) free_slots.emplace(0.0, k, c);
+    std::vector<double> load(cus, 0.0);
+    std::vector<int> count(cus, 0);
+    for (double w : work) {
+        Slot sl = free_slots.top();
+        free_slots.pop();
+        const int64_t c = std::get<2>(sl);
+        load[c] += w;
+        ++count[c];
+        free_slots.emplace(std::get<0>(sl) + w, std::get<1>(sl), c);
+    }
+    double t_max = 0;
+    for (int64_t c = 0; c < cus; ++c)
+        t_max = std::max(t_max, load[c] / (per_cu == 2 && count[c] == 1 ? 0.9 : 1.0));
+    return {pl.waves == 4 ? 1 : 0, t_max * static_cast<double>(cus) / total};
+}
+
 int cell(int64_t x, int64_t base) {
     int k = 0;
     for (int64_t v = 1; v < x; v *= base) ++k;
@@ -125,7 +200,10 @@ int cell(int64_t x, int64_t base) {
 }  // namespace
 
 struct mw_predictor {
-    std::map<std::pair<int, int>, Model> models;  // (phase, cus) -> model
+    // (phase, cus) -> model; phase 0 = prefill (8-wave path, or every prefill
+    // call without a launch shape), 1 = decode, 2 = prefill on the 4-wave path
+    std::map<std::pair<int, int>, Model> models;
+    int hkv = 0, group = 0;  // launch shape (0: plain Eq. (1) terms)
 };
 
 struct mw_guard {
@@ -156,13 +234,42 @@ static mw_status add_sample(mw_predictor *p, int phase, int32_t cus, const doubl
     return MW_OK;
 }
 
+mw_status mw_predictor_set_launch_shape(mw_predictor *p, int32_t num_q_heads, int32_t num_kv_heads) {
+    const char *who = "mw_predictor_set_launch_shape";
+    if (!p || num_kv_heads < 1 || num_q_heads < 1 || num_q_heads % num_kv_heads)
+        return fail(MW_ERR_INVALID_ARG, "%s: bad arguments", who);
+    for (const auto &kv : p->models)
+        if (kv.first.first != 1 && !kv.second.t.empty())
+            return fail(MW_ERR_INVALID_ARG, "%s: prefill samples were added before the shape", who);
+    p->hkv = num_kv_heads;
+    p->group = num_q_heads / num_kv_heads;
+    return MW_OK;
+}
+
+// Eq. (1) terms of a prefill call and the model they belong to: with a launch
+// shape, the n^2, n r and n terms are scaled by the launch's load-imbalance
+// factor and the kernel path picks the model.
+static bool prefill_sample(const mw_predictor *p, int32_t cus, int32_t batch, const int32_t *nl, const int32_t *rl,
+                           double x[4], int *phase) {
+    if (!prefill_terms(batch, nl, rl, x)) return false;
+    *phase = 0;
+    if (p->hkv > 0) {
+        const PrefillLaunch l = prefill_launch(batch, nl, rl, p->hkv, p->group, cus);
+        for (int c = 0; c < 3; ++c) x[c] *= l.kappa;
+        *phase = l.path == 0 ? 0 : 2;
+    }
+    return true;
+}
+
 mw_status mw_predictor_add_prefill(mw_predictor *p, int32_t cus, int32_t batch, const int32_t *new_lens,
                                    const int32_t *prefix_lens, double ms) {
     const char *who = "mw_predictor_add_prefill";
     double x[4];
-    if (!p || cus < 1 || batch < 1 || !new_lens || !prefix_lens || !prefill_terms(batch, new_lens, prefix_lens, x))
+    int phase = 0;
+    if (!p || cus < 1 || batch < 1 || !new_lens || !prefix_lens ||
+        !prefill_sample(p, cus, batch, new_lens, prefix_lens, x, &phase))
         return fail(MW_ERR_INVALID_ARG, "%s: bad arguments", who);
-    return add_sample(p, 0, cus, x, kPrefillTerms, ms, who);
+    return add_sample(p, phase, cus, x, kPrefillTerms, ms, who);
 }
 
 mw_status mw_predictor_add_decode(mw_predictor *p, int32_t cus, int32_t batch, const int32_t *seq_lens, double ms) {
@@ -179,9 +286,15 @@ mw_status mw_predictor_fit(mw_predictor *p) {
     for (auto &kv : p->models) {
         Model &m = kv.second;
         if (static_cast<int>(m.t.size()) < m.terms) continue;
-        if (!fit_relative(m))
+        if (!fit_relative(m)) {
+            // the 4-wave path's few samples on a small partition (calls that
+            // short are all alike) may leave its model open: that path then
+            // uses the 8-wave path's model
+            if (kv.first.first == 2) continue;
             return fail(MW_ERR_INVALID_ARG, "mw_predictor_fit: the %s samples on %d CUs do not determine the model",
-                        kv.first.first == 0 ? "prefill" : "decode", kv.first.second);
+                        kv.first.first == 1 ? "decode" : kv.first.first == 0 ? "prefill" : "4-wave prefill",
+                        kv.first.second);
+        }
         ++fitted;
     }
     return fitted ? MW_OK : fail(MW_ERR_NOT_READY, "mw_predictor_fit: no model has enough samples");
@@ -190,6 +303,8 @@ mw_status mw_predictor_fit(mw_predictor *p) {
 static mw_status predict(const mw_predictor *p, int phase, int32_t cus, const double *x, double *ms,
                          const char *who) {
     auto it = p->models.find({phase, cus});
+    if ((it == p->models.end() || !it->second.fitted) && phase != 1)  // the other prefill path's model
+        it = p->models.find({phase == 0 ? 2 : 0, cus});
     if (it == p->models.end() || !it->second.fitted)
         return fail(MW_ERR_NOT_READY, "%s: no fitted model for %d CUs", who, cus);
     double s = 0;
@@ -202,9 +317,11 @@ mw_status mw_predictor_prefill_ms(const mw_predictor *p, int32_t cus, int32_t ba
                                   const int32_t *prefix_lens, double *ms) {
     const char *who = "mw_predictor_prefill_ms";
     double x[4];
-    if (!p || !ms || batch < 1 || !new_lens || !prefix_lens || !prefill_terms(batch, new_lens, prefix_lens, x))
+    int phase = 0;
+    if (!p || !ms || cus < 1 || batch < 1 || !new_lens || !prefix_lens ||
+        !prefill_sample(p, cus, batch, new_lens, prefix_lens, x, &phase))
         return fail(MW_ERR_INVALID_ARG, "%s: bad arguments", who);
-    return predict(p, 0, cus, x, ms, who);
+    return predict(p, phase, cus, x, ms, who);
 }
 
 mw_status mw_predictor_decode_ms(const mw_predictor *p, int32_t cus, int32_t batch, const int32_t *seq_lens,
@@ -217,7 +334,7 @@ mw_status mw_predictor_decode_ms(const mw_predictor *p, int32_t cus, int32_t bat
 }
 
 mw_status mw_predictor_coefficients(const mw_predictor *p, int32_t phase, int32_t cus, double theta[4]) {
-    if (!p || !theta || (phase != 0 && phase != 1))
+    if (!p || !theta || phase < 0 || phase > 2)
         return fail(MW_ERR_INVALID_ARG, "mw_predictor_coefficients: bad arguments");
     auto it = p->models.find({phase, cus});
     if (it == p->models.end() || !it->second.fitted)

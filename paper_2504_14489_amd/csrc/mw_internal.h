@@ -129,6 +129,11 @@ struct PrefillPlan {
 // `cus` CUs (block pairing and, with allow_small, the work-group size depend
 // on it).
 mw_status prefill_prepare(const mw_prefill_args *a, int64_t cus, bool allow_small, PrefillPlan *p, const char *who);
+// The launch plan of a prefill call from its lengths alone (no validation):
+// waves, pairing and grid width for a stream of `cus` CUs; used by
+// prefill_prepare and by the latency predictor, which simulates the launch.
+void prefill_plan_lengths(int32_t batch, const int32_t *h_new_lens, int hkv, int group, int64_t cus,
+                          bool allow_small, PrefillPlan *p);
 // Plans the key-range split of a 4-wave call on `cus` CUs (cus = 0: the
 // largest split any stream could take); fills pieces, piece_tiles, rows and
 // split_bytes.  Lengths must have been validated.

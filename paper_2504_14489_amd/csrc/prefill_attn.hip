@@ -180,12 +180,22 @@ mw_status prefill_prepare(const mw_prefill_args *a, int64_t cus, bool allow_smal
         return fail(MW_ERR_INVALID_ARG, "%s: NULL device pointer", who);
     if (max_n > 0 && (!aligned16(a->d_q) || !aligned16(a->d_out)))
         return fail(MW_ERR_INVALID_ARG, "%s: Q and O must be 16-byte aligned", who);
-    p->hkv = shape->num_kv_heads;
-    p->group = shape->num_q_heads / p->hkv;
-    p->n_hgroups = (p->group + 3) / 4;
-    p->batch = a->batch;
+    prefill_plan_lengths(a->batch, a->h_new_lens, shape->num_kv_heads, shape->num_q_heads / shape->num_kv_heads, cus,
+                         allow_small, p);
     p->table_in_lds = max_pages <= kBtCache;
     p->scale_log2 = shape->scale * kLog2e;
+    if (p->gx > 0x7fffffff) return fail(MW_ERR_UNSUPPORTED, "%s: grid too large", who);
+    return MW_OK;
+}
+
+void prefill_plan_lengths(int32_t batch, const int32_t *h_new_lens, int hkv, int group, int64_t cus,
+                          bool allow_small, PrefillPlan *p) {
+    p->hkv = hkv;
+    p->group = group;
+    p->n_hgroups = (group + 3) / 4;
+    p->batch = batch;
+    p->table_in_lds = true;
+    p->scale_log2 = 0.f;
     p->paired = 0;
     p->gx = 0;
     p->pieces = 1;
@@ -193,8 +203,10 @@ mw_status prefill_prepare(const mw_prefill_args *a, int64_t cus, bool allow_smal
     p->rows = 0;
     p->split_bytes = 0;
     p->waves = 8;
-    if (max_n == 0) return MW_OK;
-    auto pairs_of = [&](int64_t bm) { return prefill_pairs(a->batch, a->h_new_lens, bm) * p->hkv * p->n_hgroups; };
+    int64_t max_n = 0;
+    for (int32_t b = 0; b < batch; ++b) max_n = std::max<int64_t>(max_n, h_new_lens[b]);
+    if (max_n == 0) return;
+    auto pairs_of = [&](int64_t bm) { return prefill_pairs(batch, h_new_lens, bm) * p->hkv * p->n_hgroups; };
     // Eight waves (64-position blocks, one work-group per CU) unless their pairs
     // would not even give every CU one: then four waves (32-position blocks,
     // two work-groups per CU), which doubles the work-groups.
@@ -212,8 +224,6 @@ mw_status prefill_prepare(const mw_prefill_args *a, int64_t cus, bool allow_smal
     const int64_t rounds = (n_pairs + slots - 1) / slots;
     p->paired = n_pairs >= slots && rounds * slots * 20 <= n_pairs * 21;
     p->gx = (p->paired ? (max_qblocks + 1) / 2 : max_qblocks) * p->hkv * p->n_hgroups;
-    if (p->gx > 0x7fffffff) return fail(MW_ERR_UNSUPPORTED, "%s: grid too large", who);
-    return MW_OK;
 }
 
 }  // namespace mw

@@ -166,6 +166,8 @@ class Estimate:
         self.model = prof["model"]
         self.p = mw.mw_predictor_create()
         self.g = mw.mw_guard_create()
+        # prefill models over the simulated launch of the profiled shape
+        mw.mw_predictor_set_launch_shape(self.p, self.model["num_q_heads"], self.model["num_kv_heads"])
         for smp in prof["prefill"]:
             if smp["grid"]:
                 mw.mw_predictor_add_prefill(self.p, smp["cus"], [smp["n"]], [smp["r"]], smp["ms"])

@@ -141,6 +141,7 @@ _SIGNATURES = {
     "mw_decode_attn_noalloc": ([_P, ctypes.POINTER(_AttnShape), _I, _PI, _P, _P, _I, _P, _P, _I, _P], _I),
     "mw_predictor_create": ([ctypes.POINTER(_P)], _I),
     "mw_predictor_destroy": ([_P], _I),
+    "mw_predictor_set_launch_shape": ([_P, _I, _I], _I),
     "mw_predictor_add_prefill": ([_P, _I, _I, _PI, _PI, ctypes.c_double], _I),
     "mw_predictor_add_decode": ([_P, _I, _I, _PI, ctypes.c_double], _I),
     "mw_predictor_fit": ([_P], _I),
@@ -442,6 +443,10 @@ def mw_predictor_create():
 
 def mw_predictor_destroy(p):
     _check(load().mw_predictor_destroy(p))
+
+
+def mw_predictor_set_launch_shape(p, num_q_heads: int, num_kv_heads: int):
+    _check(load().mw_predictor_set_launch_shape(p, int(num_q_heads), int(num_kv_heads)))
 
 
 def mw_predictor_add_prefill(p, cus: int, new_lens, prefix_lens, ms: float):

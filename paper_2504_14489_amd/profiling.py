@@ -181,6 +181,10 @@ def write_table(result, path, command):
              "sequence) per partition.  Solo = median of the calls alone on the partition's CUs; decode = whole "
              "call (split + combine kernels, balanced split).", "",
              "## Solo-run predictor (Eqs. (1)-(2), least squares of the relative error)", "",
+             "Prefill: Eq. (1) with its n^2, n r and n terms multiplied by the call's load-imbalance factor (its "
+             "launch on the partition simulated: work-groups in dispatch order, each to the CU slot that frees "
+             "first), one model per kernel path (8-wave 64-position blocks; 4-wave 32-position blocks with the "
+             "key-range split).  Decode: Eq. (2) as is.", "",
              "| phase | CUs | theta (ms per unit) | max deviation, grid (train) | max deviation, held out | "
              "held out, calls with a work-group per CU |",
              "|---|---|---|---|---|---|"]
@@ -190,6 +194,8 @@ def write_table(result, path, command):
             e = result["predictor"][phase][str(c)] if str(c) in result["predictor"][phase] \
                 else result["predictor"][phase][c]
             th = ", ".join(f"{x:.3g}" for x in e["theta"][:nth])
+            if phase == "prefill" and len(e["theta"]) >= 8:
+                th = f"8-wave: {th}; 4-wave: " + ", ".join(f"{x:.3g}" for x in e["theta"][4:8])
             lines.append(f"| {phase} | {c} | {th} | {100 * e['max_dev']['train']:.1f}% | "
                          f"{100 * e['max_dev']['held_out']:.1f}% | "
                          f"{100 * e['max_dev'].get('held_out_filling', float('nan')):.1f}% |")
@@ -228,6 +234,9 @@ def fit_and_score(samples, train_filter, phase):
     p = mw.mw_predictor_create()
     out = {}
     try:
+        # prefill: Eq. (1) over the simulated launch of this shape, one model
+        # per kernel path (8-wave or 4-wave blocks)
+        mw.mw_predictor_set_launch_shape(p, HQ, HKV)
         for s in samples:
             if not train_filter(s):
                 continue
@@ -237,7 +246,13 @@ def fit_and_score(samples, train_filter, phase):
                 mw.mw_predictor_add_decode(p, s["cus"], s["lens"], s["ms"])
         mw.mw_predictor_fit(p)
         for cus in sorted({s["cus"] for s in samples}):
-            th = mw.mw_predictor_coefficients(p, phase, cus)
+            paths = (0, 2) if phase == 0 else (1,)
+            th = []
+            for ph in paths:  # a path without a model: zeros
+                try:
+                    th += list(mw.mw_predictor_coefficients(p, ph, cus))
+                except mw.MWError:
+                    th += [0.0] * 4
             dev = {"train": 0.0, "held_out": 0.0, "held_out_filling": 0.0}
             for s in samples:
                 if s["cus"] != cus:

@@ -207,3 +207,104 @@ def test_engine_estimate_from_a_profile(tmp_path):
         assert slow == pytest.approx(1.17)
     finally:
         est.close()
+
+
+# ------------------------------- launch-imbalance factor (not from the paper)
+def test_oracle_launch_imbalance_hand_cases():
+    # 64 new tokens, 1 kv head of 1 query head, 2 CUs: the one 64-position pair
+    # is fewer than the CUs -> 32-position blocks, two work-groups per CU; the two
+    # blocks (1 key tile each) land on different CUs, each alone: factor 1 / 0.9
+    path, k = E.prefill_launch([64], [0], 1, 1, 2)
+    assert path == 1 and k == pytest.approx(1 / 0.9, rel=1e-12)
+    # 128 tokens on 1 CU: 64-position blocks 1 and 0 paired in one work-group
+    # (2 + 1 tiles): nothing to balance
+    path, k = E.prefill_launch([128], [0], 1, 1, 1)
+    assert path == 0 and k == pytest.approx(1.0, rel=1e-12)
+    # 192 tokens on 2 CUs: pairs (2, 0) with 3 + 1 tiles and (1) alone with 2:
+    # CU loads 4 and 2 against 3 each if even -> 4 * 2 / 6
+    path, k = E.prefill_launch([192], [0], 1, 1, 2)
+    assert path == 0 and k == pytest.approx(4 / 3, rel=1e-12)
+    # one 32-position block over 4064 cached tokens (64 tiles) on 4 CUs: cut in 8
+    # pieces of 8 tiles, two per CU -> even
+    path, k = E.prefill_launch([32], [4064], 1, 1, 4)
+    assert path == 1 and k == pytest.approx(1.0, rel=1e-12)
+    # 8 kv heads of 4 query heads, 4096 tokens on 64 CUs: 32 pairs x 8 heads = 256
+    # equal pairs fill 4 whole rounds -> even
+    path, k = E.prefill_launch([4096], [0], 8, 4, 64)
+    assert path == 0 and k == pytest.approx(1.0, rel=1e-12)
+
+
+def test_oracle_launch_imbalance_at_least_one():
+    rng = np.random.default_rng(5)
+    for _ in range(60):
+        bs = int(rng.integers(1, 4))
+        n = rng.integers(1, 2500, bs); r = rng.integers(0, 9000, bs)
+        cus = int(rng.choice([8, 32, 96, 256]))
+        _, k = E.prefill_launch(n, r, int(rng.choice([1, 2, 8])), int(rng.choice([1, 4, 8])), cus)
+        assert k >= 1.0 - 1e-12
+
+
+def _launch_samples(rng, hkv, group, cus, count):
+    th = {0: np.array([4e-8, 2e-8, 1e-5, 0.01]), 2: np.array([6e-8, 3e-8, 2e-5, 0.015])}
+    out = []
+    for i in range(count):
+        bs = int(rng.integers(1, 3))
+        n = rng.integers(1, 300 if i % 2 else 3000, bs); r = rng.integers(0, 20000, bs)
+        ph, x = E.prefill_features_launch(n, r, hkv, group, cus)
+        out.append((ph, n, r, x, float(x @ th[ph]) * float(rng.uniform(0.95, 1.05))))
+    return out
+
+
+def test_predictor_launch_shape_matches_oracle():
+    rng = np.random.default_rng(11)
+    hq, hkv = 32, 8
+    p = mw.mw_predictor_create()
+    try:
+        mw.mw_predictor_add_decode(p, 64, [100, 200], 0.02)  # decode samples may come first
+        mw.mw_predictor_set_launch_shape(p, hq, hkv)
+        samples = {}
+        for cus in (32, 128):
+            for ph, n, r, x, t in _launch_samples(rng, hkv, hq // hkv, cus, 40):
+                samples.setdefault((ph, cus), []).append((n, r, x, t))
+                mw.mw_predictor_add_prefill(p, cus, n, r, t)
+        mw.mw_predictor_fit(p)
+        assert {k[0] for k in samples} == {0, 2}
+        for (ph, cus), smp in samples.items():
+            assert len(smp) >= 4
+            ref = E.fit_relative(np.array([s[2] for s in smp]), np.array([s[3] for s in smp]))
+            np.testing.assert_allclose(mw.mw_predictor_coefficients(p, ph, cus), ref, rtol=1e-7)
+            for n, r, x, _ in smp[:4]:
+                assert mw.mw_predictor_prefill_ms(p, cus, n, r) == pytest.approx(float(x @ ref), rel=1e-9)
+    finally:
+        mw.mw_predictor_destroy(p)
+
+
+def test_predictor_launch_shape_rules_and_fallback():
+    p = mw.mw_predictor_create()
+    try:
+        with pytest.raises(mw.MWError):
+            mw.mw_predictor_set_launch_shape(p, 30, 8)  # not a multiple of the kv heads
+        mw.mw_predictor_set_launch_shape(p, 32, 8)
+        rng = np.random.default_rng(2)
+        smp = []
+        for _ in range(8):  # long chunks only: every sample on the 8-wave path
+            n = [int(rng.integers(6000, 9000))]; r = [int(rng.integers(0, 4000))]
+            ph, x = E.prefill_features_launch(n, r, 8, 4, 64)
+            assert ph == 0
+            t = float(x @ np.array([3e-8, 1e-8, 2e-5, 0.02]))
+            smp.append((x, t))
+            mw.mw_predictor_add_prefill(p, 64, n, r, t)
+        with pytest.raises(mw.MWError):
+            mw.mw_predictor_set_launch_shape(p, 32, 8)  # prefill samples already added
+        mw.mw_predictor_fit(p)
+        ref = E.fit_relative(np.array([s[0] for s in smp]), np.array([s[1] for s in smp]))
+        # a short chunk takes the 4-wave path, which has no model: the 8-wave
+        # path's model is used with the short chunk's own (scaled) terms
+        ph, x = E.prefill_features_launch([100], [500], 8, 4, 64)
+        assert ph == 2
+        assert mw.mw_predictor_prefill_ms(p, 64, [100], [500]) == pytest.approx(float(x @ ref), rel=1e-9)
+        with pytest.raises(mw.MWError) as ei:
+            mw.mw_predictor_coefficients(p, 2, 64)
+        assert ei.value.status == mw.MW_ERR_NOT_READY
+    finally:
+        mw.mw_predictor_destroy(p)
