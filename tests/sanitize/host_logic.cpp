@@ -1,6 +1,7 @@
 // The library's host logic on randomised inputs, for a build with
 // AddressSanitizer and UndefinedBehaviorSanitizer: the decode and prefill
-// launch planners, the page allocator and the estimator.  Nothing here
+// launch planners, the page allocator and the estimator (with the prefill
+// launch simulation).  Nothing here
 // launches a kernel or touches a GPU: the device pointers are host addresses
 // the planners only check for alignment.  Prints "ok" when every check holds.
 #include <cstdio>
@@ -172,6 +173,32 @@ void estimator() {
     }
     mw_predictor_destroy(p);
     mw_guard_destroy(g);
+    // prefill models over the simulated launch: random shapes, batches and
+    // partitions; every prediction of a fitted model is finite
+    const int hkvs[4] = {1, 2, 4, 8};
+    for (int shape = 0; shape < 6; ++shape) {
+        mw_predictor *q = nullptr;
+        check(mw_predictor_create(&q) == MW_OK, "launch-shape predictor create", shape);
+        const int hkv = hkvs[uniform(0, 3)], group = uniform(1, 16);
+        check(mw_predictor_set_launch_shape(q, hkv * group, hkv) == MW_OK, "set launch shape", shape);
+        for (int it = 0; it < 60; ++it) {
+            const int cus = 8 * uniform(1, 32), batch = uniform(1, 6);
+            std::vector<int32_t> n(batch), r(batch);
+            for (int b = 0; b < batch; ++b) {
+                n[b] = uniform(1, 6000);
+                r[b] = uniform(0, 70000);
+            }
+            mw_predictor_add_prefill(q, cus, batch, n.data(), r.data(), 0.01 + uniform(0, 100000) * 1e-4);
+            if (it % 20 == 19) {
+                mw_predictor_fit(q);
+                double out = 0.0, th[4];
+                if (mw_predictor_prefill_ms(q, cus, batch, n.data(), r.data(), &out) == MW_OK)
+                    check(out == out && out < 1e30 && out > -1e30, "launch-shape prediction finite", it);
+                mw_predictor_coefficients(q, 2 * uniform(0, 1), cus, th);
+            }
+        }
+        mw_predictor_destroy(q);
+    }
 }
 
 }  // namespace
