@@ -367,8 +367,10 @@ mw_status mw_decode_attn_noalloc(const mw_kv_pool *pool, const mw_attn_shape *sh
  *       run at once, bound by the longest.  With the shape, each prefill
  *       call's launch on `cus` CUs is planned as mw_prefill_attn_ws plans it
  *       (key-range split included) and simulated: the work-groups in dispatch
- *       order, each to the CU slot that frees first, a work-group's work its
- *       key tiles.  The n^2, n r and n terms of Eq. (1) are multiplied by the
+ *       order, each to a CU slot that frees within 5% of the mean
+ *       work-group's work of the earliest one, preferring the CU that holds
+ *       the fewest work-groups so far (work-groups a tile or two apart finish
+ *       together), a work-group's work its key tiles.  The n^2, n r and n terms of Eq. (1) are multiplied by the
  *       load-imbalance factor (the latest CU's time over the time of the same
  *       work spread evenly), and the kernel path (8-wave or 4-wave blocks)
  *       selects one of two models per partition size, fitted separately, as

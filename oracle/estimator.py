@@ -107,11 +107,15 @@ def prefill_launch(new_lens, prefix_lens, hkv: int, group: int, cus: int) -> Tup
     ceil((r + min(q bm + bm, n)) / 64) key tiles.
 
     Dispatch: grid x fastest, then the sequence; grid x enumerates pairs (or
-    blocks) times heads (times pieces, piece fastest, for the split); each
-    work-group goes to the free slot with the earliest free time (ties: the
-    lower slot index on its CU, then the lower CU), and occupies it for its
-    work in tiles.  A CU that holds one work-group of a two-per-CU launch takes
-    its work / 0.9.  Factor = max CU time * cus / total work."""
+    blocks) times heads (times pieces, piece fastest, for the split).  Each
+    work-group goes to a slot that frees no later than the earliest free time
+    plus a window of 5% of the mean work-group's work, and among those to the
+    CU that holds the fewest work-groups so far (then the lower slot index on
+    its CU, then the lower CU): work-groups that differ by a tile or two finish
+    together in practice, and the next ones spread over the CUs that freed.
+    The slot stays busy for the work-group's work in tiles.  A CU that holds
+    one work-group of a two-per-CU launch takes its work / 0.9.  Factor = max
+    CU time (the sum of its work-groups' work) * cus / total work."""
     ng = (group + 3) // 4
     heads = hkv * ng
     lens = list(zip([int(n) for n in new_lens], [int(r) for r in prefix_lens]))
@@ -169,11 +173,13 @@ def prefill_launch(new_lens, prefix_lens, hkv: int, group: int, cus: int) -> Tup
     total = float(sum(work))
     if total <= 0:
         return path, 1.0
+    window = 0.05 * total / len(work)
     free = [[0.0, k, c] for k in range(per_cu) for c in range(cus)]
     load = [0.0] * cus
     count = [0] * cus
     for w in work:
-        s = min(free, key=lambda e: (e[0], e[1], e[2]))
+        t0 = min(e[0] for e in free)
+        s = min((e for e in free if e[0] <= t0 + window), key=lambda e: (count[e[2]], e[1], e[2]))
         load[s[2]] += w
         count[s[2]] += 1
         s[0] += w

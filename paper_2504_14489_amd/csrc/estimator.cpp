@@ -6,6 +6,7 @@
 #include <cmath>
 #include <map>
 #include <queue>
+#include <set>
 #include <tuple>
 #include <vector>
 
@@ -171,19 +172,49 @@ PrefillLaunch prefill_launch(int32_t batch, const int32_t *nl, const int32_t *rl
     double total = 0;
     for (double w : work) total += w;
     if (!(total > 0)) return {pl.waves == 4 ? 1 : 0, 1.0};
-    using Slot = std::tuple<double, int, int64_t>;  // free time, slot index on its CU, CU
-    std::priority_queue<Slot, std::vector<Slot>, std::greater<Slot>> free_slots;
-    for (int k = 0; k < per_cu; ++k)
-        for (int64_t c = 0; c < cus; ++c) free_slots.emplace(0.0, k, c);
+    // Dispatch: each work-group goes to a slot that frees within a window (5%
+    // of the mean work-group's work) of the earliest free time, and among those
+    // to the CU holding the fewest work-groups so far, then the lower slot
+    // index, then the lower CU: work-groups a tile or two apart finish together
+    // on the GPU and the next ones spread over the CUs that freed.  The
+    // earliest free time never decreases, so a slot inside the window stays
+    // there until it takes a work-group.
+    const double window = 0.05 * total / static_cast<double>(work.size());
+    const int64_t nslots = per_cu * cus;  // slot = k * cus + c
+    std::vector<double> t_free(nslots, 0.0);
+    std::vector<char> in_window(nslots, 0);
+    using Timed = std::pair<double, int64_t>;  // free time, slot
+    std::priority_queue<Timed, std::vector<Timed>, std::greater<Timed>> later;
+    std::set<std::tuple<int, int, int64_t>> ready;  // (work-groups on the CU, slot index, CU)
+    std::multiset<double> ready_t;
+    for (int64_t sl = 0; sl < nslots; ++sl) later.emplace(0.0, sl);
     std::vector<double> load(cus, 0.0);
     std::vector<int> count(cus, 0);
     for (double w : work) {
-        Slot sl = free_slots.top();
-        free_slots.pop();
-        const int64_t c = std::get<2>(sl);
-        load[c] += w;
+        double t0 = later.empty() ? INFINITY : later.top().first;
+        if (!ready_t.empty()) t0 = std::min(t0, *ready_t.begin());
+        while (!later.empty() && later.top().first <= t0 + window) {
+            const int64_t sl = later.top().second;
+            later.pop();
+            ready.emplace(count[sl % cus], static_cast<int>(sl / cus), sl % cus);
+            ready_t.insert(t_free[sl]);
+            in_window[sl] = 1;
+        }
+        const auto pick = *ready.begin();
+        ready.erase(ready.begin());
+        const int k = std::get<1>(pick);
+        const int64_t c = std::get<2>(pick), sl = k * cus + c;
+        ready_t.erase(ready_t.find(t_free[sl]));
+        in_window[sl] = 0;
+        for (int k2 = 0; k2 < per_cu; ++k2)  // the CU's other slots in the window move to its new count
+            if (k2 != k && in_window[k2 * cus + c]) {
+                ready.erase(std::make_tuple(count[c], k2, c));
+                ready.emplace(count[c] + 1, k2, c);
+            }
         ++count[c];
-        free_slots.emplace(std::get<0>(sl) + w, std::get<1>(sl), c);
+        load[c] += w;
+        t_free[sl] += w;
+        later.emplace(t_free[sl], sl);
     }
     double t_max = 0;
     for (int64_t c = 0; c < cus; ++c)

@@ -123,7 +123,7 @@ def pair_slowdown(pre: PrefillCall, dec: DecodeCall, part: Partition, pre_ms: fl
     """Decode calls back to back on the decode CUs with prefill calls next to
     them (decode enqueued first); the decode calls that ran entirely inside
     the prefill window give the multiplexed latency."""
-    n_pre = min(256, max(1, math.ceil(3 * dec_ms / pre_ms)))
+    n_pre = min(1024, max(1, math.ceil(3 * dec_ms / pre_ms)))
     n_dec = min(512, math.ceil(n_pre * pre_ms / dec_ms) + 3)
     td = [Timing() for _ in range(n_dec)]
     tp = [Timing() for _ in range(n_pre)]
@@ -182,8 +182,8 @@ def write_table(result, path, command):
              "call (split + combine kernels, balanced split).", "",
              "## Solo-run predictor (Eqs. (1)-(2), least squares of the relative error)", "",
              "Prefill: Eq. (1) with its n^2, n r and n terms multiplied by the call's load-imbalance factor (its "
-             "launch on the partition simulated: work-groups in dispatch order, each to the CU slot that frees "
-             "first), one model per kernel path (8-wave 64-position blocks; 4-wave 32-position blocks with the "
+             "launch on the partition simulated: work-groups in dispatch order, each to a CU slot that frees within "
+             "5% of a work-group's work of the first one, the CU holding the fewest work-groups first), one model per kernel path (8-wave 64-position blocks; 4-wave 32-position blocks with the "
              "key-range split).  Decode: Eq. (2) as is.", "",
              "| phase | CUs | theta (ms per unit) | max deviation, grid (train) | max deviation, held out | "
              "held out, calls with a work-group per CU |",
@@ -280,23 +280,24 @@ def main(argv=None):
     ap.add_argument("--prefill-cus", default="32,64,96,128,160,192,224")
     ap.add_argument("--reps", type=int, default=5)
     ap.add_argument("--held-out", type=int, default=20, help="random held-out samples per partition and phase")
-    ap.add_argument("--guard-reused", default="0,4096,16384,65536",
+    ap.add_argument("--guard-reused", default="0,4096,16384,65536,131072",
                     help="prefill reused tokens of the contention-guard pairs")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--quick", action="store_true", help="a small grid (functional check)")
     ap.add_argument("--table", default="", help="also write the Markdown summary here")
     args = ap.parse_args(argv)
     torch.cuda.init()
-    # the predictor's grid: powers of 2 in new tokens and batch size, powers
-    # of 4 in reused tokens and context; the contention guard's pairs take the
-    # powers of 4 (the paper's grid) within it
+    # the predictor's grid: powers of 2 in new tokens, powers of 4 in reused
+    # tokens and context (reused up to 128K), 16 batch sizes from 1 to 256;
+    # the contention guard's pairs take the powers of 4 within it and every
+    # batch size (the paper samples about 20)
     grid_n = [256, 512, 1024, 2048, 4096, 8192, 16384]
-    grid_r = [0, 1024, 4096, 16384, 65536]
-    grid_bs = [1, 2, 4, 8, 16, 32, 64, 128, 256]
+    grid_r = [0, 1024, 4096, 16384, 65536, 131072]
+    grid_bs = [1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64, 96, 128, 192, 256]
     grid_L = [256, 1024, 4096, 16384, 65536]
     guard_n = [1024, 4096, 16384]
     guard_r = [int(x) for x in args.guard_reused.split(",")]
-    guard_bs = [8, 32, 128]
+    guard_bs = grid_bs
     guard_L = [1024, 4096, 16384, 65536]
     max_dec_tokens = 2 ** 22          # decode samples hold at most this many cached tokens (16 GB of K/V)
     if args.quick:

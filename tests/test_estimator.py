@@ -234,6 +234,25 @@ def test_oracle_launch_imbalance_hand_cases():
     assert path == 0 and k == pytest.approx(1.0, rel=1e-12)
 
 
+def test_oracle_launch_dispatch_window():
+    # 141 tokens over 3000 cached, 2 kv heads, 3 CUs: 4 pairs do not fill 2 whole
+    # rounds of 3 -> single 64-position blocks 2, 2, 1, 1, 0, 0 (heads fastest) of
+    # 50, 50, 49, 49, 48, 48 tiles; window 0.05 * 294 / 6.  Work-groups 0-2 take
+    # CUs 0-2 (free at 50, 50, 49); work-group 3 sees all three inside the window,
+    # equal counts -> CU 0; then CU 1, CU 2: loads 99, 98, 97 (the earliest-free
+    # rule alone would give 98 each)
+    path, k = E.prefill_launch([141], [3000], 2, 1, 3)
+    assert path == 0 and k == pytest.approx(99 * 3 / 294, rel=1e-12)
+    # 130 tokens over 576 cached, 1 kv head, 6 CUs: 32-position blocks cut into
+    # pieces, 15 work-groups of 4,4,4,3,4,4 | 3,4,4,3,3,4 | 3,3,4 tiles (54 in all)
+    # on 12 slots.  The first 12 fill slot 0 then slot 1 of CUs 0-5; at time 3 the
+    # free slots are slot 0 of CU 3 and slot 1 of CUs 0, 3, 4, every CU holding 2:
+    # CU 3, then CU 0 (2 < 3), then CU 4 (2 < 3) -> loads 10, 8, 8, 9, 11, 8 and
+    # 11 * 6 / 54 (the lower-slot rule alone gives CU 3 both tail work-groups: 13)
+    path, k = E.prefill_launch([130], [576], 1, 1, 6)
+    assert path == 1 and k == pytest.approx(11 * 6 / 54, rel=1e-12)
+
+
 def test_oracle_launch_imbalance_at_least_one():
     rng = np.random.default_rng(5)
     for _ in range(60):
@@ -275,6 +294,30 @@ def test_predictor_launch_shape_matches_oracle():
             np.testing.assert_allclose(mw.mw_predictor_coefficients(p, ph, cus), ref, rtol=1e-7)
             for n, r, x, _ in smp[:4]:
                 assert mw.mw_predictor_prefill_ms(p, cus, n, r) == pytest.approx(float(x @ ref), rel=1e-9)
+    finally:
+        mw.mw_predictor_destroy(p)
+
+
+def test_predictor_launch_shape_long_prefixes_match_oracle():
+    # split launches over long prefixes, where many work-groups tie
+    rng = np.random.default_rng(17)
+    p = mw.mw_predictor_create()
+    try:
+        mw.mw_predictor_set_launch_shape(p, 32, 8)
+        th = np.array([5e-8, 2e-8, 3e-5, 0.02])
+        smp = []
+        for _ in range(12):
+            n = [int(rng.integers(100, 1500))]; r = [int(rng.integers(0, 60000))]
+            ph, x = E.prefill_features_launch(n, r, 8, 4, 96)
+            assert ph == 2
+            t = float(x @ th) * float(rng.uniform(0.95, 1.05))
+            smp.append((n, r, x, t))
+            mw.mw_predictor_add_prefill(p, 96, n, r, t)
+        mw.mw_predictor_fit(p)
+        ref = E.fit_relative(np.array([s[2] for s in smp]), np.array([s[3] for s in smp]))
+        np.testing.assert_allclose(mw.mw_predictor_coefficients(p, 2, 96), ref, rtol=1e-7)
+        for n, r, x, _ in smp:
+            assert mw.mw_predictor_prefill_ms(p, 96, n, r) == pytest.approx(float(x @ ref), rel=1e-9)
     finally:
         mw.mw_predictor_destroy(p)
 
