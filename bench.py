@@ -5,8 +5,9 @@ One step = one pass of the whole hot path over one batch of synthetic input,
 with the two phases on disjoint CU partitions of the GPU (decode enqueued
 first, as the paper launches the decode iteration before prefill, Sec. 3.2.2):
 
-  decode stream : m x (append each sequence's new K/V, decode attention
-                  = split kernel + combine kernel)
+  decode stream : m x (append each sequence's new K/V, decode attention:
+                  one kernel, the balanced split, whose last work-group on
+                  each (sequence, kv head) merges that segment's pieces)
   prefill stream: append each chunk's new K/V, causal prefill attention
 
 m is the number of decode iterations that fit in one prefill call when the
@@ -241,7 +242,7 @@ class Bench:
                       for row in tks],
                "kernels": tks[-1][0].kernels(),
                "call": [sum(tk.elapsed()[0] for tk in row) for row in tks]}
-        if which == "decode":
+        if which == "decode" and out["kernels"] > 1:
             out["k1"] = [row[0].kernel_ms(1) for row in tks]
         return out
 
@@ -447,7 +448,7 @@ def run_partition(b, p_cus, d_cus, p_index, args):
         "prefill_tflops": steps * b.pre_flop / wall / 1e12,
         "decode_gbs": steps * m * b.dec_bytes / wall / 1e9,
         "iso": {"prefill_kernel_ms": median(iso_p["k0"]), "decode_split_ms": median(iso_d["k0"]),
-                "decode_combine_ms": median(iso_d["k1"]), "decode_call_ms": median(iso_d["call"]),
+                "decode_kernels": iso_d["kernels"], "decode_call_ms": median(iso_d["call"]),
                 "flushed": True},
         "solo_full_gpu": {"prefill_kernel_ms": median(solo_p["k0"]), "decode_call_ms": median(solo_d["call"])},
         "mux": {"prefill_kernel_ms": median(mux["prefill_k"]), "prefill_kernel_p90_ms": p90(mux["prefill_k"]),

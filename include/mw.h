@@ -283,17 +283,21 @@ mw_status mw_prefill_attn_ws(const mw_kv_pool *pool, const mw_attn_shape *shape,
                              void *d_workspace, size_t workspace_bytes, mw_stream stream, mw_timing *timing);
 
 /* Decode streams each (sequence, kv head) segment of the K/V pages split into
- * pieces whose partial results a second kernel merges (log-sum-exp combine,
- * the flash-decoding split of Sec. 2.2's memory-bound decode).  chunk_pages
+ * pieces whose partial results are merged with the log-sum-exp combine (the
+ * flash-decoding split of Sec. 2.2's memory-bound decode).  chunk_pages
  * chooses the split:
  *   0  (default) balanced: the segments laid end to end are cut into equal
  *      ranges of pages, two per CU of the stream the call runs on (at most
- *      512, at least 8 pages each); a range may cross segment boundaries and
+ *      512, at least 16 pages each); a range may cross segment boundaries and
  *      every CU streams the same number of bytes.  The split depends on the
- *      lengths and on the stream's CU count.
+ *      lengths and on the stream's CU count.  One kernel: the work-group
+ *      that finds every piece of a segment done (per-piece flags in the
+ *      workspace, tagged per call, so the workspace needs no initialisation)
+ *      merges that segment.
  *   -1 fixed chunks chosen from the lengths: the largest of 128, 64 and 32
  *      pages that still gives at least 1024 (chunk, kv head) work units.
- *   8..256, a multiple of 8: fixed chunks of that many pages.
+ *   8..256, a multiple of 8: fixed chunks of that many pages; a second
+ *      kernel merges the chunks.
  * No split ever depends on page ids (renumbering pages changes no result).
  * Pass the same chunk_pages (and lengths) to both calls; the size for 0
  * covers both splits that chunk_pages 0 can select (see mw_fused_attn).
@@ -305,8 +309,10 @@ mw_status mw_decode_workspace_size(const mw_attn_shape *shape, int32_t batch,
  *       L_b <= bt_stride * page_size
  *   d_block_table device [batch][bt_stride]
  *   d_q, d_out device [batch][num_q_heads][head_dim] bf16
- *   d_workspace device, >= mw_decode_workspace_size bytes, 16-B aligned
- * Two kernel launches (split, combine); `timing` may be NULL. */
+ *   d_workspace device, >= mw_decode_workspace_size bytes, 16-B aligned;
+ *       two calls that run at the same time need two workspaces
+ * One kernel launch with the balanced split, two (split, combine) with fixed
+ * chunks; `timing` may be NULL. */
 mw_status mw_decode_attn(const mw_kv_pool *pool, const mw_attn_shape *shape, int32_t batch,
                          const int32_t *h_seq_lens, const int32_t *d_seq_lens,
                          const int32_t *d_block_table, int32_t bt_stride, const void *d_q,
@@ -323,7 +329,8 @@ mw_status mw_decode_attn(const mw_kv_pool *pool, const mw_attn_shape *shape, int
  * array.  A call whose split needs more than 16 MiB of workspace (see
  * mw_decode_workspace_size) fails with MW_ERR_UNSUPPORTED before launching
  * anything.  Nothing in the array needs clearing between calls: a call reads
- * only what it wrote.  Every call on a device shares its array, so calls
+ * only what it wrote (the merge's done flags count only with the call's own
+ * tag).  Every call on a device shares its array, so calls
  * that may overlap in time on one device (two streams, two threads) race:
  * order them on one stream or use mw_decode_attn.  No timing handle. */
 mw_status mw_decode_attn_noalloc(const mw_kv_pool *pool, const mw_attn_shape *shape, int32_t batch,

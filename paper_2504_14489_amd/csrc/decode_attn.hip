@@ -2,6 +2,7 @@
 // the split kernel (its work-unit body is in decode_block.h), the combine
 // kernel and their launch.
 #include <algorithm>
+#include <atomic>
 #include <mutex>
 
 #include "decode_block.h"
@@ -31,112 +32,63 @@ __global__ void __launch_bounds__(kThreads)
 k_decode_balanced(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpool,
                   const uint16_t *__restrict__ q, uint16_t *__restrict__ out,
                   const int32_t *__restrict__ seq_lens, const int32_t *__restrict__ bt, int bt_stride,
-                  float *__restrict__ ws_o, float2 *__restrict__ ws_ml, int32_t *__restrict__ ws_cbase,
-                  int batch, int hkv, int group, int num_pages, float scale_log2, int64_t per_unit,
-                  int64_t total) {
+                  float *__restrict__ ws_o, float2 *__restrict__ ws_ml, uint32_t *__restrict__ flags,
+                  uint32_t tag, int64_t slots, int batch, int hkv, int group, int num_pages, float scale_log2,
+                  int64_t per_unit, int64_t total) {
     __shared__ __attribute__((aligned(16))) uint16_t s_v[kWaves * kWaveBufElems];
     __shared__ float s_m[kWaves][16];
     __shared__ float s_l[kWaves][16];
-    decode_span(kpool, vpool, q, out, seq_lens, bt, bt_stride, ws_o, ws_ml, ws_cbase, batch, hkv, group, num_pages,
-                scale_log2, per_unit, total, blockIdx.x, threadIdx.x, s_v, s_m, s_l);
+    decode_span(kpool, vpool, q, out, seq_lens, bt, bt_stride, ws_o, ws_ml, flags, tag, slots, batch, hkv, group,
+                num_pages, scale_log2, per_unit, total, blockIdx.x, threadIdx.x, s_v, s_m, s_l);
 }
 
-// One work-group per (sequence, kv head), each thread merging two outputs
-// (h, d) of the segment's pieces.
-// Fixed chunks (per_unit = 0): chunk c of sequence b is slot
-// (ws_cbase[b] + c) hkv + kv head.  Balanced split (per_unit > 0): the
-// segment starts at global page P = ws_cbase[b] + kv head * pages(b), and its
-// pieces are those of units P / per_unit .. (P + pages(b) - 1) / per_unit,
-// unit u's piece in slot u + b hkv + kv head.
+// Combine of the fixed-chunk split: one work-group per (sequence, kv head);
+// chunk c of sequence b is in slot (ws_cbase[b] + c) hkv + kv head.  (The
+// balanced split merges its segments itself.)
 __global__ void __launch_bounds__(kThreads)
 k_decode_combine(uint16_t *__restrict__ out, const int32_t *__restrict__ seq_lens,
                  const float *__restrict__ ws_o, const float2 *__restrict__ ws_ml,
                  const int32_t *__restrict__ ws_cbase, int hkv, int group, int ch_pages, int bt_stride,
-                 int64_t per_unit, int64_t slots) {
+                 int64_t slots) {
     const int b = blockIdx.x / hkv, kvh = blockIdx.x % hkv;
-    int64_t first = 0, stride = hkv;  // slot of piece j: first + j * stride
-    int nch = 0;
-    if (per_unit > 0) {
-        const int np = chunks_of(seq_lens[b], 1, bt_stride);
-        const int64_t start = static_cast<int64_t>(ws_cbase[b]) + static_cast<int64_t>(kvh) * np;
-        if (np <= 0 || start < 0) return;
-        const int64_t u0 = start / per_unit, u1 = (start + np - 1) / per_unit;
-        nch = static_cast<int>(u1 - u0 + 1);
-        first = u0 + static_cast<int64_t>(b) * hkv + kvh;
-        stride = 1;
-    } else {
-        nch = chunks_of(seq_lens[b], ch_pages, bt_stride);
-        first = static_cast<int64_t>(ws_cbase[b]) * hkv + kvh;
-    }
+    const int nch = chunks_of(seq_lens[b], ch_pages, bt_stride);
+    const int64_t first = static_cast<int64_t>(ws_cbase[b]) * hkv + kvh;
     if (nch <= 1) return;  // written by the split kernel
     // lengths on the device that disagree with the host copy must not lead
     // outside the workspace
-    if (first < 0 || first + static_cast<int64_t>(nch - 1) * stride >= slots) return;
-    const int hq = hkv * group;
-    // One pass over the pieces with a running maximum; each thread merges two
-    // outputs (h, d), and the (m, l) and o of 8 pieces of both are loaded
-    // together, so a short segment costs one round of loads.
-    const int n_out = group * kHeadDim;
-    for (int i0 = threadIdx.x; i0 < n_out; i0 += 2 * kThreads) {
-        const int idx[2] = {i0, i0 + kThreads};
-        float M[2] = {-INFINITY, -INFINITY}, lsum[2] = {0.f, 0.f}, osum[2] = {0.f, 0.f};
-        for (int s0 = 0; s0 < nch; s0 += 8) {
-            float2 ml[2][8];
-            float o[2][8];
-#pragma unroll
-            for (int k = 0; k < 2; ++k)
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const bool in = s0 + j < nch && idx[k] < n_out;
-                    const int h = in ? idx[k] / kHeadDim : 0, d = idx[k] % kHeadDim;
-                    const size_t uu = static_cast<size_t>(first + (s0 + j) * stride) * group + h;
-                    ml[k][j] = in ? ws_ml[uu] : make_float2(-INFINITY, 0.f);
-                    o[k][j] = in ? ws_o[uu * kHeadDim + d] : 0.f;
-                }
-#pragma unroll
-            for (int k = 0; k < 2; ++k)
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    if (!(ml[k][j].y > 0.f)) continue;  // a piece without keys contributes nothing
-                    const float mn = fmaxf(M[k], ml[k][j].x);
-                    const float a = __builtin_amdgcn_exp2f(M[k] - mn), w = __builtin_amdgcn_exp2f(ml[k][j].x - mn);
-                    lsum[k] = lsum[k] * a + w * ml[k][j].y;
-                    osum[k] = osum[k] * a + w * o[k][j];
-                    M[k] = mn;
-                }
-        }
-#pragma unroll
-        for (int k = 0; k < 2; ++k)
-            if (idx[k] < n_out) {
-                const int h = idx[k] / kHeadDim, d = idx[k] % kHeadDim;
-                out[(static_cast<size_t>(b) * hq + kvh * group + h) * kHeadDim + d] = to_bf16(osum[k] / lsum[k]);
-            }
-    }
+    if (first < 0 || first + static_cast<int64_t>(nch - 1) * hkv >= slots) return;
+    merge_pieces(out, ws_o, ws_ml, first, hkv, nch, b, hkv, kvh, group, threadIdx.x);
 }
 
 // Balanced split: units per CU of the stream (two 4-wave work-groups fit a
 // CU), the most units (two per CU of a 256-CU device; the workspace is sized
-// for it) and the fewest pages a unit streams (one pair per wave).
+// for it) and the fewest pages a unit streams (two pairs per wave: short
+// calls are bound by latency, not bytes, and fewer, longer pieces leave less
+// to merge at the end).
 constexpr int64_t kBalancedPerCu = 2;
 constexpr int64_t kBalancedMaxUnits = 512;
-constexpr int64_t kBalancedMinPages = 8;
+constexpr int64_t kBalancedMinPages = 16;
 
 struct Plan {
     int64_t units;            // work-groups of the split kernel
     int chunk_pages;          // fixed chunks; 0 with the balanced split
     int64_t per_unit, total;  // balanced split: pages per unit, pages in all
     int64_t slots;            // partial slots of the workspace
-    size_t off_ml, off_cbase, bytes;
+    size_t off_ml, off_meta, bytes;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
+// Workspace: partial O [slots][group][128] and (m, l) [slots][group] in fp32,
+// then the fixed-chunk split's per-sequence chunk bases or the balanced
+// split's per-slot done flags.
 void plan_layout(Plan *plan, int32_t batch, int group) {
     const size_t o_bytes = align256(static_cast<size_t>(plan->slots) * group * kHeadDim * 4);
     const size_t ml_bytes = align256(static_cast<size_t>(plan->slots) * group * 8);
     plan->off_ml = o_bytes;
-    plan->off_cbase = o_bytes + ml_bytes;
-    plan->bytes = plan->off_cbase + align256(static_cast<size_t>(batch) * 4 + 4);
+    plan->off_meta = o_bytes + ml_bytes;
+    const size_t meta = plan->per_unit > 0 ? static_cast<size_t>(plan->slots) * 4 : static_cast<size_t>(batch) * 4 + 4;
+    plan->bytes = plan->off_meta + align256(meta);
 }
 
 // chunk_pages > 0: fixed chunks of that many pages; -1 (or 0 with cus = 0):
@@ -235,7 +187,7 @@ mw_status decode_prepare(const mw_decode_args *a, int64_t cus, DecodePlan *p, co
     p->total = pl.total;
     p->slots = pl.slots;
     p->off_ml = pl.off_ml;
-    p->off_cbase = pl.off_cbase;
+    p->off_meta = pl.off_meta;
     p->bytes = pl.bytes;
     p->hkv = shape->num_kv_heads;
     p->group = shape->num_q_heads / shape->num_kv_heads;
@@ -249,8 +201,8 @@ mw_status decode_combine_launch(const mw_decode_args *a, const DecodePlan &p, hi
     hipLaunchKernelGGL(k_decode_combine, dim3(static_cast<unsigned>(a->batch) * p.hkv), dim3(kThreads), 0, s,
                        static_cast<uint16_t *>(a->d_out), a->d_seq_lens, reinterpret_cast<const float *>(ws),
                        reinterpret_cast<const float2 *>(ws + p.off_ml),
-                       reinterpret_cast<const int32_t *>(ws + p.off_cbase), p.hkv, p.group, p.chunk_pages,
-                       a->bt_stride, p.per_unit, p.slots);
+                       reinterpret_cast<const int32_t *>(ws + p.off_meta), p.hkv, p.group, p.chunk_pages,
+                       a->bt_stride, p.slots);
     return check_launch("k_decode_combine");
 }
 
@@ -272,7 +224,17 @@ mw_status mw_decode_workspace_size(const mw_attn_shape *shape, int32_t batch, co
 
 namespace {
 
-// The split and combine launches of one planned decode call.
+// Tag of a balanced-split launch, never 0 (the cleared flag value): a done
+// flag in a workspace counts only for the launch whose tag it shows.
+std::atomic<uint32_t> g_decode_tag{0};
+uint32_t next_tag() {
+    uint32_t t = 0;
+    while (t == 0) t = g_decode_tag.fetch_add(1, std::memory_order_relaxed) + 1;
+    return t;
+}
+
+// The launches of one planned decode call: the balanced split (which merges
+// its own segments), or the fixed-chunk split and its combine.
 mw_status decode_launch(const mw_decode_args &a, const DecodePlan &pl, hipStream_t s, mw_timing *timing) {
     const mw_kv_pool *pool = a.pool;
     const int32_t batch = a.batch, bt_stride = a.bt_stride;
@@ -288,15 +250,15 @@ mw_status decode_launch(const mw_decode_args &a, const DecodePlan &pl, hipStream
                                pool->k, pool->v, static_cast<const uint16_t *>(d_q), static_cast<uint16_t *>(d_out),
                                d_seq_lens, d_block_table, bt_stride, reinterpret_cast<float *>(ws),
                                reinterpret_cast<float2 *>(ws + pl.off_ml),
-                               reinterpret_cast<int32_t *>(ws + pl.off_cbase), batch, pl.hkv, pl.group,
-                               pool->desc.num_pages, pl.scale_log2, pl.per_unit, pl.total);
+                               reinterpret_cast<uint32_t *>(ws + pl.off_meta), next_tag(), pl.slots,
+                               batch, pl.hkv, pl.group, pool->desc.num_pages, pl.scale_log2, pl.per_unit, pl.total);
             st = check_launch("k_decode_balanced");
         } else {
             hipLaunchKernelGGL(k_decode_split, dim3(static_cast<unsigned>(pl.units)), dim3(kThreads), 0, s,
                                pool->k, pool->v, static_cast<const uint16_t *>(d_q), static_cast<uint16_t *>(d_out),
                                d_seq_lens, d_block_table, bt_stride, reinterpret_cast<float *>(ws),
                                reinterpret_cast<float2 *>(ws + pl.off_ml),
-                               reinterpret_cast<int32_t *>(ws + pl.off_cbase), batch, pl.hkv, pl.group,
+                               reinterpret_cast<int32_t *>(ws + pl.off_meta), batch, pl.hkv, pl.group,
                                pool->desc.num_pages, pl.scale_log2, pl.chunk_pages);
             st = check_launch("k_decode_split");
         }
@@ -304,9 +266,11 @@ mw_status decode_launch(const mw_decode_args &a, const DecodePlan &pl, hipStream
     }
     st = timing_kernel_done(timing, s);
     if (st != MW_OK) return st;
-    st = decode_combine_launch(&a, pl, s);
-    if (st != MW_OK) return st;
-    st = timing_kernel_done(timing, s);
+    if (pl.per_unit == 0) {  // fixed chunks: the combine kernel
+        st = decode_combine_launch(&a, pl, s);
+        if (st != MW_OK) return st;
+        st = timing_kernel_done(timing, s);
+    }
     timing_end(timing);
     return st;
 }

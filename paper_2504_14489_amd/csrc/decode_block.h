@@ -27,9 +27,11 @@
 //     rescaled), which the result O / l does not depend on.
 // The 4 waves' (m, l, O) are merged in LDS at the end; a sequence that fits
 // one chunk writes its bf16 output directly, otherwise the chunk's partial goes
-// to the workspace and the combine kernel merges the chunks of each
-// (sequence, kv head) with the log-sum-exp identity
-//   M = max m_s,  O = sum 2^(m_s - M) o_s / sum 2^(m_s - M) l_s.
+// to the workspace and the pieces of each (sequence, kv head) are merged with
+// the log-sum-exp identity
+//   M = max m_s,  O = sum 2^(m_s - M) o_s / sum 2^(m_s - M) l_s
+// by the work-group that finishes the segment's last piece (balanced split)
+// or by the combine kernel (fixed chunks).
 #pragma once
 #include "mw_internal.h"
 
@@ -297,8 +299,14 @@ decode_pages(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vp
         if (direct) {
             out[(static_cast<size_t>(b) * hq + kvh * group + h) * kHeadDim + d] = to_bf16(o / lsum);
         } else {
-            ws_o[(static_cast<size_t>(slot) * group + h) * kHeadDim + d] = o;
-            if (d == 0) ws_ml[static_cast<size_t>(slot) * group + h] = make_float2(M, lsum);
+            // device-scope stores (through the L2 of this XCD): the piece may be
+            // merged by a work-group on another XCD without a cache writeback
+            __hip_atomic_store(&ws_o[(static_cast<size_t>(slot) * group + h) * kHeadDim + d], o, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+            if (d == 0)
+                __hip_atomic_store(reinterpret_cast<unsigned long long *>(&ws_ml[static_cast<size_t>(slot) * group + h]),
+                                   __builtin_bit_cast(unsigned long long, make_float2(M, lsum)), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
         }
     }
 }
@@ -362,19 +370,202 @@ __device__ bool locate_page(const int32_t *__restrict__ seq_lens, int batch, int
     return false;
 }
 
+// Merges the pieces j = 0 .. nch-1 of segment (b, kv head), piece j's partial
+// in workspace slot first + j * stride, into the bf16 output (the combine
+// kernel).  One pass over the pieces with a running maximum; each thread
+// merges two outputs (h, d), and the (m, l) and o of 8 pieces of both are
+// loaded together, so a short segment costs one round of loads.
+__device__ __forceinline__ void
+merge_pieces(uint16_t *__restrict__ out, const float *__restrict__ ws_o, const float2 *__restrict__ ws_ml,
+             int64_t first, int64_t stride, int nch, int b, int hkv, int kvh, int group, int tid) {
+    const int hq = hkv * group;
+    const int n_out = group * kHeadDim;
+    for (int i0 = tid; i0 < n_out; i0 += 2 * kThreads) {
+        const int idx[2] = {i0, i0 + kThreads};
+        float M[2] = {-INFINITY, -INFINITY}, lsum[2] = {0.f, 0.f}, osum[2] = {0.f, 0.f};
+        for (int s0 = 0; s0 < nch; s0 += 8) {
+            float2 ml[2][8];
+            float o[2][8];
+#pragma unroll
+            for (int k = 0; k < 2; ++k)
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const bool in = s0 + j < nch && idx[k] < n_out;
+                    const int h = in ? idx[k] / kHeadDim : 0, d = idx[k] % kHeadDim;
+                    const size_t uu = static_cast<size_t>(first + (s0 + j) * stride) * group + h;
+                    ml[k][j] = in ? ws_ml[uu] : make_float2(-INFINITY, 0.f);
+                    o[k][j] = in ? ws_o[uu * kHeadDim + d] : 0.f;
+                }
+#pragma unroll
+            for (int k = 0; k < 2; ++k)
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    if (!(ml[k][j].y > 0.f)) continue;  // a piece without keys contributes nothing
+                    const float mn = fmaxf(M[k], ml[k][j].x);
+                    const float a = __builtin_amdgcn_exp2f(M[k] - mn), w = __builtin_amdgcn_exp2f(ml[k][j].x - mn);
+                    lsum[k] = lsum[k] * a + w * ml[k][j].y;
+                    osum[k] = osum[k] * a + w * o[k][j];
+                    M[k] = mn;
+                }
+        }
+#pragma unroll
+        for (int k = 0; k < 2; ++k)
+            if (idx[k] < n_out) {
+                const int h = idx[k] / kHeadDim, d = idx[k] % kHeadDim;
+                out[(static_cast<size_t>(b) * hq + kvh * group + h) * kHeadDim + d] = to_bf16(osum[k] / lsum[k]);
+            }
+    }
+}
+
+// Merge of one balanced-split segment in the work-group that finished its
+// last piece; pieces j = 0 .. nch-1 in slots first + j, read at device scope
+// (they were written in this kernel, possibly on other XCDs).  First the
+// pieces' (m, l), which lie together in the workspace, all go to LDS and one
+// wave per head reduces the maximum M and the denominator
+// sum_j 2^(m_j - M) l_j; then each wave streams the partial O of one head
+// at a time, two outputs per lane with 8 pieces of both in flight, weighting
+// each piece by 2^(m_j - M).
+// s_ml holds nch * group entries (at most kMergeMaxEntries).
+constexpr int kMergeMaxEntries = kWaves * kWaveBufElems * 2 / 8;
+constexpr int kBufferFormat32 = 0x00020000;  // buffer descriptor word 3: 32-bit data format
+constexpr int kLoadDeviceScope = 16;         // buffer load cache policy: device scope
+__device__ __forceinline__ void
+merge_segment(uint16_t *__restrict__ out, const float *__restrict__ ws_o, const float2 *__restrict__ ws_ml,
+              int64_t first, int nch, int b, int hkv, int kvh, int group, int tid, float2 *s_ml, float *s_M,
+              float *s_L) {
+    const int lane = tid & 63, wave = tid >> 6;
+    const int n_ml = nch * group;
+    unsigned long long *ml_src = reinterpret_cast<unsigned long long *>(const_cast<float2 *>(ws_ml)) + first * group;
+    for (int e = tid; e < n_ml; e += kThreads)
+        s_ml[e] = __builtin_bit_cast(float2, __hip_atomic_load(ml_src + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+    __syncthreads();
+    for (int h = wave; h < group; h += kWaves) {
+        float M = -INFINITY;
+        for (int j = lane; j < nch; j += 64) {
+            const float2 v = s_ml[j * group + h];
+            if (v.y > 0.f) M = fmaxf(M, v.x);  // a piece without keys contributes nothing
+        }
+#pragma unroll
+        for (int sh = 32; sh >= 1; sh >>= 1) M = fmaxf(M, __shfl_xor(M, sh));
+        float L = 0.f;
+        for (int j = lane; j < nch; j += 64) {
+            const float2 v = s_ml[j * group + h];
+            if (v.y > 0.f) L += __builtin_amdgcn_exp2f(v.x - M) * v.y;
+        }
+#pragma unroll
+        for (int sh = 32; sh >= 1; sh >>= 1) L += __shfl_xor(L, sh);
+        if (lane == 0) {
+            s_M[h] = M;
+            s_L[h] = L;
+        }
+    }
+    __syncthreads();
+    const int hq = hkv * group;
+    const int n_out = group * kHeadDim;
+    // the pieces' partial O through a buffer resource: one offset register per
+    // output, the piece's offset in the scalar operand, device-scope loads.
+    // One wave per head, each lane two of its outputs, so a piece's weight is
+    // one broadcast LDS read for both.
+    const __amdgpu_buffer_rsrc_t r_o =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(ws_o) + static_cast<size_t>(first) * n_out, 0,
+                                          nch * n_out * 4, kBufferFormat32);
+    for (int h = wave; h < group; h += kWaves) {
+        const float M = s_M[h];
+        float acc0 = 0.f, acc1 = 0.f;
+        for (int j0 = 0; j0 < nch; j0 += 8) {
+            float o0[8], o1[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const bool in = j0 + j < nch;
+                const int off = 4 * (j0 + j) * n_out;
+                o0[j] = in ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                           r_o, 4 * (h * kHeadDim + lane), off, kLoadDeviceScope))
+                           : 0.f;
+                o1[j] = in ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                           r_o, 4 * (h * kHeadDim + 64 + lane), off, kLoadDeviceScope))
+                           : 0.f;
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                if (j0 + j >= nch) break;
+                const float2 v = s_ml[(j0 + j) * group + h];
+                const float w = v.y > 0.f ? __builtin_amdgcn_exp2f(v.x - M) : 0.f;
+                acc0 += w * o0[j];
+                acc1 += w * o1[j];
+            }
+        }
+        const float inv = 1.f / s_L[h];
+        uint16_t *orow = out + (static_cast<size_t>(b) * hq + kvh * group + h) * kHeadDim;
+        orow[lane] = to_bf16(acc0 * inv);
+        orow[64 + lane] = to_bf16(acc1 * inv);
+    }
+}
+
+// A work-group that has written its pieces of split segments (at most two:
+// the unit's first and last) marks them done in their flags (this call's
+// tag) and reads the segments' other flags, both segments in one round; a
+// work-group that finds every piece of a segment done merges the segment and
+// clears its flags.  The work-group that marks last always finds them all;
+// two that finish together may both merge, writing the same bits.  Pieces
+// and flags are written and read with device-scope stores and loads
+// (coherent across the XCDs' L2 caches), and each wave waits for its stores
+// to complete before the next step; release/acquire fences would instead
+// write back and invalidate the whole L2 of the XCD for every work-group, and
+// one counter per segment would serialise the pieces' atomics.  A flag from an
+// earlier call shows another tag (tags are never 0, the cleared value), so
+// the workspace needs no initialisation, and a replay of the same launch (same
+// tag) finds the flags cleared.  No work-group waits for another.
+__device__ __forceinline__ void
+finish_segments(uint16_t *__restrict__ out, const float *__restrict__ ws_o, const float2 *__restrict__ ws_ml,
+                uint32_t *__restrict__ flags, uint32_t tag, int npend, const int64_t *first, const int *nch,
+                const int64_t *self, const int *sb, const int *skvh, int64_t slots, int hkv, int group, int tid,
+                float2 *s_ml, float *s_M, float *s_L) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's piece stores are complete
+    __syncthreads();
+    if (tid == 0) {
+        for (int i = 0; i < npend; ++i)
+            if (self[i] >= 0 && self[i] < slots)
+                __hip_atomic_store(flags + self[i], tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
+    __syncthreads();
+    // both segments' flags in one round of loads; device lengths that
+    // disagree with the host's must not lead outside the workspace
+    bool ok[2], done[2] = {true, true};
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        ok[i] = i < npend && first[i] >= 0 && first[i] + nch[i] - 1 < slots && nch[i] * group <= kMergeMaxEntries;
+        for (int j = tid; ok[i] && j < nch[i]; j += kThreads)
+            done[i] &= __hip_atomic_load(flags + first[i] + j, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == tag;
+    }
+    const bool all0 = __syncthreads_and(ok[0] && done[0]);
+    const bool all1 = __syncthreads_and(ok[1] && done[1]);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        if (!(i == 0 ? all0 : all1)) continue;
+        for (int j = tid; j < nch[i]; j += kThreads)
+            __hip_atomic_store(flags + first[i] + j, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (i == 1 && all0) __syncthreads();  // the first merge is done with the LDS
+        merge_segment(out, ws_o, ws_ml, first[i], nch[i], sb[i], hkv, skvh[i], group, tid, s_ml, s_M, s_L);
+    }
+}
+
 // One unit of the balanced split: global pages [u R, min((u + 1) R, total))
 // of the (sequence, kv head) segments in order, which may cross segment
 // boundaries.  Each segment piece is merged on its own: a segment the unit
 // holds whole is written directly, a piece of a longer segment goes to slot
-// u + s (s = b hkv + kv head), and the unit that starts sequence b writes
-// hkv * (pages of sequences < b) to ws_cbase[b] for the combine kernel.
+// u + s (s = b hkv + kv head) with its done flag in `flags` at the same
+// index, and the work-group that finds every piece of the segment done
+// merges them (those of units P / R .. (P + pages(b) - 1) / R, P the
+// segment's first global page).
 // Not for fused work-groups: the number of barriers depends on the unit.
 __device__ __forceinline__ void
 decode_span(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpool,
             const uint16_t *__restrict__ q, uint16_t *__restrict__ out, const int32_t *__restrict__ seq_lens,
             const int32_t *__restrict__ bt, int bt_stride, float *__restrict__ ws_o, float2 *__restrict__ ws_ml,
-            int32_t *__restrict__ ws_cbase, int batch, int hkv, int group, int num_pages, float scale_log2,
-            int64_t per_unit, int64_t total, int u, int tid, uint16_t *s_v, float (*s_m)[16], float (*s_l)[16]) {
+            uint32_t *__restrict__ flags, uint32_t tag, int64_t slots, int batch, int hkv, int group,
+            int num_pages, float scale_log2, int64_t per_unit, int64_t total, int u, int tid, uint16_t *s_v,
+            float (*s_m)[16], float (*s_l)[16]) {
     int64_t g = static_cast<int64_t>(u) * per_unit;
     const int64_t g_end = min(g + per_unit, total);
     int b = 0;
@@ -384,13 +575,29 @@ decode_span(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpo
     int np_b = (L + kPageSize - 1) / kPageSize;
     int kvh = static_cast<int>((g - base_b) / np_b);
     int off = static_cast<int>((g - base_b) % np_b);
+    // the unit's pieces of split segments (only its first and last piece can
+    // be): counted in and merged after all its pages, when none of the page
+    // loop's registers are live any more
+    int pend_b[2] = {0, 0}, pend_kvh[2] = {0, 0}, pend_nch[2] = {0, 0}, npend = 0;
+    int64_t pend_first[2] = {0, 0}, pend_self[2] = {0, 0};
     for (bool first = true; g < g_end; first = false) {
         const int n = static_cast<int>(min(static_cast<int64_t>(np_b - off), g_end - g));
-        if (!first) __syncthreads();  // the previous piece's merge is done with the LDS
+        if (!first) __syncthreads();  // the previous piece is done with the LDS
+        const bool whole = off == 0 && n == np_b;
+        const int64_t seg = static_cast<int64_t>(b) * hkv + kvh;
         decode_pages(kpool, vpool, q, out, bt + static_cast<size_t>(b) * bt_stride, ws_o, ws_ml, b, L, hkv, kvh,
-                     group, num_pages, scale_log2, off, off + n, true, off == 0 && n == np_b,
-                     static_cast<int64_t>(u) + static_cast<int64_t>(b) * hkv + kvh, tid, s_v, s_m, s_l);
-        if (off == 0 && kvh == 0 && tid == 0) ws_cbase[b] = static_cast<int32_t>(base_b);
+                     group, num_pages, scale_log2, off, off + n, true, whole, static_cast<int64_t>(u) + seg, tid, s_v,
+                     s_m, s_l);
+        if (!whole && npend < 2) {
+            const int64_t p0 = base_b + static_cast<int64_t>(kvh) * np_b;
+            const int64_t u0 = p0 / per_unit, u1 = (p0 + np_b - 1) / per_unit;
+            pend_b[npend] = b;
+            pend_kvh[npend] = kvh;
+            pend_first[npend] = u0 + seg;
+            pend_self[npend] = static_cast<int64_t>(u) + seg;
+            pend_nch[npend] = static_cast<int>(u1 - u0 + 1);
+            ++npend;
+        }
         g += n;
         off = 0;
         if (++kvh == hkv) {
@@ -402,6 +609,9 @@ decode_span(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpo
             if (np_b == 0) break;  // device lengths that disagree with the host's
         }
     }
+    if (npend > 0)
+        finish_segments(out, ws_o, ws_ml, flags, tag, npend, pend_first, pend_nch, pend_self, pend_b, pend_kvh, slots,
+                        hkv, group, tid, reinterpret_cast<float2 *>(s_v), s_m[0], s_l[0]);
 }
 
 }  // namespace dk

@@ -94,7 +94,7 @@ extern "C" mw_status mw_fused_attn(const mw_prefill_args *pre, const mw_decode_a
                            static_cast<int>(pp.gx > 0 ? pp.gx : 1), n_pre, static_cast<const uint16_t *>(dec->d_q),
                            static_cast<uint16_t *>(dec->d_out), dec->d_seq_lens, dec->d_block_table, dec->bt_stride,
                            reinterpret_cast<float *>(ws), reinterpret_cast<float2 *>(ws + dp.off_ml),
-                           reinterpret_cast<int32_t *>(ws + dp.off_cbase), dec->batch, dp.group, dp.scale_log2,
+                           reinterpret_cast<int32_t *>(ws + dp.off_meta), dec->batch, dp.group, dp.scale_log2,
                            dp.chunk_pages, n_dec);
         st = check_launch("k_fused_attn");
         if (st != MW_OK) return st;

@@ -100,7 +100,9 @@ struct DecodePlan {
     int64_t per_unit;     // balanced split: pages per unit (0 with fixed chunks)
     int64_t total;        // balanced split: pages of all (sequence, kv head) segments
     int64_t slots;        // partial slots in the workspace
-    size_t off_ml, off_cbase, bytes;  // workspace layout: partial O, (m, l), per-sequence bases
+    // workspace layout: partial O, (m, l), then per-sequence chunk bases (fixed
+    // chunks) or per-slot done flags (balanced split)
+    size_t off_ml, off_meta, bytes;
     int hkv, group;
     float scale_log2;
 };
@@ -108,7 +110,8 @@ struct DecodePlan {
 // cus > 0 with chunk_pages = 0: the balanced split over that many CUs;
 // cus = 0: fixed chunks only (chunk_pages 0 then means automatic chunks).
 mw_status decode_prepare(const mw_decode_args *a, int64_t cus, DecodePlan *p, const char *who);
-// Launches the kernel that merges the chunk partials of every (sequence, kv head).
+// Launches the kernel that merges the chunk partials of every (sequence, kv
+// head) of a fixed-chunk split (the balanced split merges its own).
 mw_status decode_combine_launch(const mw_decode_args *a, const DecodePlan &p, hipStream_t s);
 
 // Checked launch parameters of one prefill call.

@@ -154,11 +154,11 @@ def pair_slowdown(pre: PrefillCall, dec: DecodeCall, part: Partition, pre_ms: fl
 def work_groups(sample, phase) -> int:
     """Work-groups of the call: query blocks of 64 positions x kv heads for
     prefill; for decode the balanced split's page ranges (two per CU, at
-    least 8 pages each)."""
+    least 16 pages each)."""
     if phase == 0:
         return (sample["n"] + 63) // 64 * HKV
     pages = sum((L + PAGE - 1) // PAGE for L in sample["lens"]) * HKV
-    return min(2 * sample["cus"], (pages + 7) // 8)
+    return min(2 * sample["cus"], (pages + 15) // 16)
 
 
 def write_table(result, path, command):
@@ -179,7 +179,7 @@ def write_table(result, path, command):
              + ", ".join(f"{p}/{256 - p}" for p in pcus) + ".  "
              f"Held-out samples: {held} random prefill (n, r) and {held} random decode batches (random lengths per "
              "sequence) per partition.  Solo = median of the calls alone on the partition's CUs; decode = whole "
-             "call (split + combine kernels, balanced split).", "",
+             "call (balanced split, one kernel that also merges).", "",
              "## Solo-run predictor (Eqs. (1)-(2), least squares of the relative error)", "",
              "Prefill: Eq. (1) with its n^2, n r and n terms multiplied by the call's load-imbalance factor (its "
              "launch on the partition simulated: work-groups in dispatch order, each to a CU slot that frees within "

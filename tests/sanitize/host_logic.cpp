@@ -63,7 +63,10 @@ void planners() {
         if (st == MW_OK && st2 == MW_OK) {
             check(dp.bytes <= bytes, "the workspace size covers the split of every CU count", it);
             check(dp.units >= 0 && dp.slots >= dp.units, "plan counts", it);
-            check(dp.off_ml <= dp.off_cbase && dp.off_cbase <= dp.bytes, "workspace layout", it);
+            check(dp.off_ml <= dp.off_meta && dp.off_meta <= dp.bytes, "workspace layout", it);
+            // per-sequence chunk bases, or the balanced split's per-slot done flags
+            const size_t meta = dp.per_unit > 0 ? static_cast<size_t>(dp.slots) * 4 : static_cast<size_t>(batch) * 4;
+            check(dp.off_meta + meta <= dp.bytes, "workspace holds the flags", it);
         }
         if (st != MW_OK) check(st2 != MW_OK, "a refused size is refused by the plan too", it);
         // prefill: varlen batches, prefixes, tables that are too short

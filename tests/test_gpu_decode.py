@@ -180,3 +180,53 @@ def test_decode_ignores_nan_and_inf_in_slack_slots(slack, chunk_pages):
     got = run_decode(wl, chunk_pages)
     ref = oracle.decode(wl.q_dec, wl.k_pool, wl.v_pool, wl.dec_bt, wl.dec_lens)
     assert_close(got, ref, f"decode slack chunk_pages={chunk_pages}")
+
+
+def test_decode_segment_flags_with_any_workspace_contents():
+    """The balanced split merges each (sequence, kv head) in the work-group
+    that finds all of its pieces done, through per-piece flags in the
+    workspace: the result must not depend on what the workspace held before
+    (never written, all ones, random bytes, an earlier call's flags)."""
+    say("decode segment flags: workspace contents")
+    cfg = W.custom_config(hq=32, hkv=8, pre_chunks=((0, 1),), dec_batch=5, dec_len_lo=2000,
+                          dec_len_hi=9000, seed=51)
+    wl = W.make_workload(cfg)
+    ref = oracle.decode(wl.q_dec, wl.k_pool, wl.v_pool, wl.dec_bt, wl.dec_lens)
+    dw = DeviceWorkload(wl)
+    try:
+        ws = dw.workspace(0)
+        gen = torch.Generator(device=dw.device).manual_seed(3)
+        results = []
+        for fill in ("as allocated", "ones", "random", "reused", "reused"):
+            if fill == "ones":
+                ws.fill_(255)
+            elif fill == "random":
+                ws.copy_(torch.randint(0, 256, ws.shape, generator=gen, device=dw.device, dtype=torch.uint8))
+            dw.o_dec.zero_()
+            got = to_bits(dw.decode())
+            torch.cuda.synchronize()
+            assert_close(got, ref, f"decode, workspace {fill}")
+            results.append(got)
+        for got in results[1:]:
+            assert np.array_equal(got, results[0]), "the result depends on the workspace contents"
+    finally:
+        dw.close()
+
+
+def test_decode_one_segment_in_hundreds_of_pieces():
+    """One sequence, one kv head: the whole call is a single segment cut into
+    as many pieces as the split has units (hundreds of flags per merge)."""
+    say("decode one segment, many pieces")
+    cfg = W.custom_config(hq=16, hkv=1, pre_chunks=((0, 1),), dec_batch=1, dec_len_lo=70001,
+                          dec_len_hi=70002, seed=52)
+    wl = W.make_workload(cfg)
+    ref = oracle.decode(wl.q_dec, wl.k_pool, wl.v_pool, wl.dec_bt, wl.dec_lens)
+    dw = DeviceWorkload(wl)
+    try:
+        for rep in range(3):
+            dw.o_dec.zero_()
+            got = to_bits(dw.decode())
+            torch.cuda.synchronize()
+            assert_close(got, ref, f"decode one segment, call {rep}")
+    finally:
+        dw.close()
