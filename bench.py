@@ -370,7 +370,7 @@ def roofline_entries(b, res):
     medians of the timed multiplexed region; returns (dominant, other)."""
     n_launch = len(b.chunks)
     pre_ms = res["mux"]["prefill_kernel_ms"] / n_launch
-    dec_ms = res["mux"]["decode_split_ms"]
+    dec_ms = res["mux"]["decode_kernel_ms"]
     split = res["mux"]["prefill_kernels"] > 1   # key-range split: split + merge kernels per call
     pre = {"kernel": "k_prefill_split+k_prefill_merge" if split else "k_prefill_attn", "bound": "mfma",
            "unit": "TFLOP/s",
@@ -447,13 +447,13 @@ def run_partition(b, p_cus, d_cus, p_index, args):
         "ms_per_step": 1e3 * wall / steps,
         "prefill_tflops": steps * b.pre_flop / wall / 1e12,
         "decode_gbs": steps * m * b.dec_bytes / wall / 1e9,
-        "iso": {"prefill_kernel_ms": median(iso_p["k0"]), "decode_split_ms": median(iso_d["k0"]),
+        "iso": {"prefill_kernel_ms": median(iso_p["k0"]), "decode_kernel_ms": median(iso_d["k0"]),
                 "decode_kernels": iso_d["kernels"], "decode_call_ms": median(iso_d["call"]),
                 "flushed": True},
         "solo_full_gpu": {"prefill_kernel_ms": median(solo_p["k0"]), "decode_call_ms": median(solo_d["call"])},
         "mux": {"prefill_kernel_ms": median(mux["prefill_k"]), "prefill_kernel_p90_ms": p90(mux["prefill_k"]),
                 "prefill_kernels": mux["prefill_kernels"],
-                "decode_split_ms": median(mux["decode_k0"]), "decode_call_ms": median(mux["decode_call"]),
+                "decode_kernel_ms": median(mux["decode_k0"]), "decode_call_ms": median(mux["decode_call"]),
                 "decode_call_p90_ms": p90(mux["decode_call"]),
                 "prefill_window_ms": mux["prefill_window_ms"], "decode_window_ms": mux["decode_window_ms"]},
         "mux_equals_isolated_bitwise": same,
@@ -606,7 +606,7 @@ def traffic_pass(args):
 
 def tables(entries):
     """Markdown: one row per workload (its first split), then the sweep."""
-    rows = ["| workload | CUs pre/dec | prefill kernel (mux) | TFLOP/s | % share | % MFMA ceiling | decode split (mux) | "
+    rows = ["| workload | CUs pre/dec | prefill kernel (mux) | TFLOP/s | % share | % MFMA ceiling | decode kernel (mux) | "
             "GB/s | % stream ceiling | % of 8 TB/s | slowdown pre / dec | mux = iso | parity max-abs |",
             "|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
     for e in entries.values():
