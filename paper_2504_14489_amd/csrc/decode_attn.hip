@@ -1,6 +1,7 @@
 // Decode attention: one query token per sequence over its paged context --
-// the split kernel (its work-unit body is in decode_block.h), the combine
-// kernel and their launch.
+// the balanced split kernel, which merges its own split segments, the
+// fixed-chunk split kernel and its combine kernel (their bodies are in
+// decode_block.h), and their launch.
 #include <algorithm>
 #include <atomic>
 #include <mutex>
