@@ -289,8 +289,11 @@ mw_status mw_prefill_attn_ws(const mw_kv_pool *pool, const mw_attn_shape *shape,
  *   0  (default) balanced: the segments laid end to end are cut into equal
  *      ranges of pages, two per CU of the stream the call runs on (at most
  *      512, at least 16 pages each); a range may cross segment boundaries and
- *      every CU streams the same number of bytes.  The split depends on the
- *      lengths and on the stream's CU count.  One kernel: the work-group
+ *      every CU streams the same number of bytes (when every sequence is
+ *      long enough for two ranges or more, segments are padded to a multiple
+ *      of the range instead, so that ranges do not straddle segments, if that
+ *      keeps 90% of the work-groups).  The split depends on the lengths and
+ *      on the stream's CU count.  One kernel: the work-group
  *      that finds every piece of a segment done (per-piece flags in the
  *      workspace, tagged per call, so the workspace needs no initialisation)
  *      merges that segment.

@@ -3,6 +3,7 @@
 // fixed-chunk split kernel and its combine kernel (their bodies are in
 // decode_block.h), and their launch.
 #include <algorithm>
+#include <climits>
 #include <atomic>
 #include <mutex>
 
@@ -35,12 +36,12 @@ k_decode_balanced(const uint16_t *__restrict__ kpool, const uint16_t *__restrict
                   const int32_t *__restrict__ seq_lens, const int32_t *__restrict__ bt, int bt_stride,
                   float *__restrict__ ws_o, float2 *__restrict__ ws_ml, uint32_t *__restrict__ flags,
                   uint32_t tag, int64_t slots, int batch, int hkv, int group, int num_pages, float scale_log2,
-                  int64_t per_unit, int64_t total) {
+                  int64_t per_unit, int64_t total, int aligned) {
     __shared__ __attribute__((aligned(16))) uint16_t s_v[kWaves * kWaveBufElems];
     __shared__ float s_m[kWaves][16];
     __shared__ float s_l[kWaves][16];
     decode_span(kpool, vpool, q, out, seq_lens, bt, bt_stride, ws_o, ws_ml, flags, tag, slots, batch, hkv, group,
-                num_pages, scale_log2, per_unit, total, blockIdx.x, threadIdx.x, s_v, s_m, s_l);
+                num_pages, scale_log2, per_unit, total, aligned != 0, blockIdx.x, threadIdx.x, s_v, s_m, s_l);
 }
 
 // Combine of the fixed-chunk split: one work-group per (sequence, kv head);
@@ -73,7 +74,8 @@ constexpr int64_t kBalancedMinPages = 16;
 struct Plan {
     int64_t units;            // work-groups of the split kernel
     int chunk_pages;          // fixed chunks; 0 with the balanced split
-    int64_t per_unit, total;  // balanced split: pages per unit, pages in all
+    int64_t per_unit, total;  // balanced split: pages per unit, pages in all (of the split's numbering)
+    bool aligned;             // balanced split: segments padded to multiples of per_unit
     int64_t slots;            // partial slots of the workspace
     size_t off_ml, off_meta, bytes;
 };
@@ -131,14 +133,55 @@ mw_status plan_decode(const mw_attn_shape *shape, int32_t batch, const int32_t *
         pl->chunk_pages = ch;
         pl->units = pl->slots = count(ch) * hkv;
         pl->per_unit = pl->total = 0;
+        pl->aligned = false;
         plan_layout(pl, batch, group);
     };
-    auto balanced = [&](int64_t n_cus, Plan *pl) {
+    // may_align = false for workspace sizing: an aligned split needs no more
+    // units than the unaligned one on as many CUs, whose count only grows with
+    // the CUs
+    auto balanced = [&](int64_t n_cus, Plan *pl, bool may_align) {
         pl->chunk_pages = 0;
         pl->total = count(1) * hkv;
         int64_t units = std::min(kBalancedPerCu * std::max<int64_t>(n_cus, 1), kBalancedMaxUnits);
         units = std::max<int64_t>(1, std::min(units, (pl->total + kBalancedMinPages - 1) / kBalancedMinPages));
         pl->per_unit = std::max<int64_t>(1, (pl->total + units - 1) / units);
+        // Few long segments (each cut into two pieces or more): pad every
+        // segment to a multiple of the range, so that a unit holds one piece
+        // of one segment (a range that straddles two segments costs a second
+        // piece set-up and a second merge at the end).  The range is the
+        // shortest one, no shorter than the balanced one, whose padded
+        // segments need no more units than the balanced split (equal segments
+        // are then cut in equal pieces); padding is used only if it keeps at
+        // least 90% of those units busy.
+        pl->aligned = false;
+        int64_t np_min = INT64_MAX, np_max = 0;
+        for (int32_t b = 0; b < batch; ++b) {
+            const int64_t np = (h_seq_lens[b] + kPageSize - 1) / kPageSize;
+            np_min = std::min(np_min, np);
+            np_max = std::max(np_max, np);
+        }
+        const int64_t units_bal = (pl->total + pl->per_unit - 1) / pl->per_unit;
+        auto padded_units = [&](int64_t r) {
+            int64_t n = 0;
+            for (int32_t b = 0; b < batch; ++b) n += ((h_seq_lens[b] + kPageSize - 1) / kPageSize + r - 1) / r;
+            return n * hkv;
+        };
+        if (may_align && batch > 0 && np_min >= 2 * pl->per_unit) {
+            int64_t lo = pl->per_unit, hi = np_max;  // padded_units(np_max) = batch * hkv <= units_bal / 2
+            while (lo < hi) {
+                const int64_t mid = lo + (hi - lo) / 2;
+                if (padded_units(mid) <= units_bal)
+                    hi = mid;
+                else
+                    lo = mid + 1;
+            }
+            const int64_t n = padded_units(lo);
+            if (10 * n >= 9 * units_bal) {
+                pl->aligned = true;
+                pl->per_unit = lo;
+                pl->total = n * lo;
+            }
+        }
         pl->units = pl->total > 0 ? (pl->total + pl->per_unit - 1) / pl->per_unit : 0;
         // piece of unit u of segment s in slot u + s
         pl->slots = pl->units > 0 ? pl->units + static_cast<int64_t>(batch) * hkv - 1 : 0;
@@ -148,10 +191,10 @@ mw_status plan_decode(const mw_attn_shape *shape, int32_t batch, const int32_t *
         // workspace for either split of chunk_pages = 0
         Plan a, b;
         fixed(0, &a);
-        balanced(kBalancedMaxUnits, &b);
+        balanced(kBalancedMaxUnits, &b, false);
         *plan = a.bytes >= b.bytes ? a : b;
     } else if (chunk_pages == 0 && cus > 0) {
-        balanced(cus, plan);
+        balanced(cus, plan, true);
     } else {
         fixed(chunk_pages, plan);
     }
@@ -186,6 +229,7 @@ mw_status decode_prepare(const mw_decode_args *a, int64_t cus, DecodePlan *p, co
     p->chunk_pages = pl.chunk_pages;
     p->per_unit = pl.per_unit;
     p->total = pl.total;
+    p->aligned = pl.aligned;
     p->slots = pl.slots;
     p->off_ml = pl.off_ml;
     p->off_meta = pl.off_meta;
@@ -252,7 +296,8 @@ mw_status decode_launch(const mw_decode_args &a, const DecodePlan &pl, hipStream
                                d_seq_lens, d_block_table, bt_stride, reinterpret_cast<float *>(ws),
                                reinterpret_cast<float2 *>(ws + pl.off_ml),
                                reinterpret_cast<uint32_t *>(ws + pl.off_meta), next_tag(), pl.slots,
-                               batch, pl.hkv, pl.group, pool->desc.num_pages, pl.scale_log2, pl.per_unit, pl.total);
+                               batch, pl.hkv, pl.group, pool->desc.num_pages, pl.scale_log2, pl.per_unit, pl.total,
+                               pl.aligned ? 1 : 0);
             st = check_launch("k_decode_balanced");
         } else {
             hipLaunchKernelGGL(k_decode_split, dim3(static_cast<unsigned>(pl.units)), dim3(kThreads), 0, s,

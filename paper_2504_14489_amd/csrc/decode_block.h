@@ -342,15 +342,18 @@ decode_unit(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpo
 
 // Wave-level search for the sequence b whose kv-head segments hold global
 // page g of the balanced split (segments in the order (b, kv head), each of
-// the sequence's page count); base_out = hkv * (pages of sequences < b).
-// Returns false if g is past the end.
-__device__ bool locate_page(const int32_t *__restrict__ seq_lens, int batch, int bt_stride, int hkv, int64_t g,
-                            int &b_out, int64_t &base_out) {
+// the sequence's page count, rounded up to a multiple of `align` when it is
+// not 0); base_out = hkv * (such counts of the sequences < b).  Returns false
+// if g is past the end.
+__device__ bool locate_page(const int32_t *__restrict__ seq_lens, int batch, int bt_stride, int hkv, int64_t align,
+                            int64_t g, int &b_out, int64_t &base_out) {
     const int lane = threadIdx.x & 63;
     int64_t running = 0;
     for (int base = 0; base < batch; base += 64) {
         const int bb = base + lane;
-        const int64_t n = bb < batch ? static_cast<int64_t>(hkv) * chunks_of(seq_lens[bb], 1, bt_stride) : 0;
+        int64_t np = bb < batch ? chunks_of(seq_lens[bb], 1, bt_stride) : 0;
+        if (align > 0) np = (np + align - 1) / align * align;
+        const int64_t n = static_cast<int64_t>(hkv) * np;
         int64_t x = n;
 #pragma unroll
         for (int off = 1; off < 64; off <<= 1) {
@@ -552,7 +555,9 @@ finish_segments(uint16_t *__restrict__ out, const float *__restrict__ ws_o, cons
 
 // One unit of the balanced split: global pages [u R, min((u + 1) R, total))
 // of the (sequence, kv head) segments in order, which may cross segment
-// boundaries.  Each segment piece is merged on its own: a segment the unit
+// boundaries; with `aligned`, every segment is padded to a multiple of R
+// pages (the padding holds no pages), so a unit holds one piece of one
+// segment.  Each segment piece is merged on its own: a segment the unit
 // holds whole is written directly, a piece of a longer segment goes to slot
 // u + s (s = b hkv + kv head) with its done flag in `flags` at the same
 // index, and the work-group that finds every piece of the segment done
@@ -564,33 +569,39 @@ decode_span(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpo
             const uint16_t *__restrict__ q, uint16_t *__restrict__ out, const int32_t *__restrict__ seq_lens,
             const int32_t *__restrict__ bt, int bt_stride, float *__restrict__ ws_o, float2 *__restrict__ ws_ml,
             uint32_t *__restrict__ flags, uint32_t tag, int64_t slots, int batch, int hkv, int group,
-            int num_pages, float scale_log2, int64_t per_unit, int64_t total, int u, int tid, uint16_t *s_v,
-            float (*s_m)[16], float (*s_l)[16]) {
+            int num_pages, float scale_log2, int64_t per_unit, int64_t total, bool aligned, int u, int tid,
+            uint16_t *s_v, float (*s_m)[16], float (*s_l)[16]) {
     int64_t g = static_cast<int64_t>(u) * per_unit;
     const int64_t g_end = min(g + per_unit, total);
     int b = 0;
     int64_t base_b = 0;
-    if (g >= g_end || !locate_page(seq_lens, batch, bt_stride, hkv, g, b, base_b)) return;
+    const int64_t align = aligned ? per_unit : 0;
+    if (g >= g_end || !locate_page(seq_lens, batch, bt_stride, hkv, align, g, b, base_b)) return;
     int L = min(seq_lens[b], bt_stride * kPageSize);
     int np_b = (L + kPageSize - 1) / kPageSize;
-    int kvh = static_cast<int>((g - base_b) / np_b);
-    int off = static_cast<int>((g - base_b) % np_b);
+    // the segment's extent in the split's page numbering (padded when aligned)
+    auto extent = [&](int np) { return aligned ? static_cast<int>((np + align - 1) / align * align) : np; };
+    int nv_b = extent(np_b);
+    int kvh = static_cast<int>((g - base_b) / nv_b);
+    int off = static_cast<int>((g - base_b) % nv_b);
     // the unit's pieces of split segments (only its first and last piece can
     // be): counted in and merged after all its pages, when none of the page
     // loop's registers are live any more
     int pend_b[2] = {0, 0}, pend_kvh[2] = {0, 0}, pend_nch[2] = {0, 0}, npend = 0;
     int64_t pend_first[2] = {0, 0}, pend_self[2] = {0, 0};
     for (bool first = true; g < g_end; first = false) {
-        const int n = static_cast<int>(min(static_cast<int64_t>(np_b - off), g_end - g));
+        // n pages of the split's numbering, of which those below np_b exist
+        const int n = static_cast<int>(min(static_cast<int64_t>(nv_b - off), g_end - g));
+        const int p_end = min(off + n, np_b);
         if (!first) __syncthreads();  // the previous piece is done with the LDS
-        const bool whole = off == 0 && n == np_b;
+        const bool whole = off == 0 && p_end == np_b && n == nv_b;
         const int64_t seg = static_cast<int64_t>(b) * hkv + kvh;
         decode_pages(kpool, vpool, q, out, bt + static_cast<size_t>(b) * bt_stride, ws_o, ws_ml, b, L, hkv, kvh,
-                     group, num_pages, scale_log2, off, off + n, true, whole, static_cast<int64_t>(u) + seg, tid, s_v,
+                     group, num_pages, scale_log2, off, p_end, true, whole, static_cast<int64_t>(u) + seg, tid, s_v,
                      s_m, s_l);
         if (!whole && npend < 2) {
-            const int64_t p0 = base_b + static_cast<int64_t>(kvh) * np_b;
-            const int64_t u0 = p0 / per_unit, u1 = (p0 + np_b - 1) / per_unit;
+            const int64_t p0 = base_b + static_cast<int64_t>(kvh) * nv_b;
+            const int64_t u0 = p0 / per_unit, u1 = (p0 + nv_b - 1) / per_unit;
             pend_b[npend] = b;
             pend_kvh[npend] = kvh;
             pend_first[npend] = u0 + seg;
@@ -602,10 +613,11 @@ decode_span(const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpo
         off = 0;
         if (++kvh == hkv) {
             kvh = 0;
-            base_b += static_cast<int64_t>(hkv) * np_b;
+            base_b += static_cast<int64_t>(hkv) * nv_b;
             if (++b >= batch) break;
             L = min(seq_lens[b], bt_stride * kPageSize);
             np_b = (L + kPageSize - 1) / kPageSize;
+            nv_b = extent(np_b);
             if (np_b == 0) break;  // device lengths that disagree with the host's
         }
     }

@@ -98,7 +98,8 @@ struct DecodePlan {
     int64_t units;        // work-groups of the split kernel
     int chunk_pages;      // fixed chunks: resolved chunk length; 0 with the balanced split
     int64_t per_unit;     // balanced split: pages per unit (0 with fixed chunks)
-    int64_t total;        // balanced split: pages of all (sequence, kv head) segments
+    int64_t total;        // balanced split: pages of all (sequence, kv head) segments, in the split's numbering
+    bool aligned;         // balanced split: each segment padded to a multiple of per_unit pages
     int64_t slots;        // partial slots in the workspace
     // workspace layout: partial O, (m, l), then per-sequence chunk bases (fixed
     // chunks) or per-slot done flags (balanced split)

@@ -127,8 +127,12 @@ def test_decode_wide_score_range():
 
 # (name, hq, hkv, batch, shortest, longest): long sequences whose segments the
 # balanced ranges cut, and many 1..3-page sequences several of whose segments
-# fall in one range
-BALANCED_CASES = [("long", 32, 8, 24, 1, 3000), ("short", 8, 2, 300, 1, 40), ("group16", 16, 1, 5, 700, 4100)]
+# fall in one range; then few long sequences, whose segments the split pads to
+# a multiple of the range (one sequence of 139 pages, a prime; one of 34 pages,
+# cut 16 + 16 + 2; three of unequal lengths)
+BALANCED_CASES = [("long", 32, 8, 24, 1, 3000), ("short", 8, 2, 300, 1, 40), ("group16", 16, 1, 5, 700, 4100),
+                  ("one139", 32, 8, 1, 2213, 2213), ("one34", 32, 8, 1, 530, 530),
+                  ("three", 32, 8, 3, 9000, 20000)]
 
 
 @pytest.mark.parametrize("decode_cus", [8, 64, 192, 256])
