@@ -234,3 +234,40 @@ def test_decode_one_segment_in_hundreds_of_pieces():
             assert_close(got, ref, f"decode one segment, call {rep}")
     finally:
         dw.close()
+
+
+def test_decode_random_batches_on_partitions():
+    """Random small batches (1-6 sequences of 1..20000 tokens, equal or not)
+    with random head shapes on random partition sizes: whichever balanced
+    split the planner takes (ranges across segments, or segments padded to
+    whole ranges), the result is the oracle's."""
+    from paper_2504_14489_amd.device import Partition
+    rng = np.random.default_rng(77)
+    for case in range(12):
+        hkv = int(rng.choice([1, 2, 8]))
+        hq = hkv * int(rng.choice([1, 4, 8]))
+        batch = int(rng.integers(1, 7))
+        if case % 3 == 0:
+            lens = [int(rng.integers(1, 20001))] * batch
+        else:
+            lens = [int(x) for x in rng.integers(1, 20001, batch)]
+        decode_cus = int(rng.choice([8, 32, 96, 160, 256]))
+        say(f"decode random case {case}: hq={hq} hkv={hkv} lens={lens} on {decode_cus} CUs")
+        cfg = W.custom_config(hq=hq, hkv=hkv, pre_chunks=((0, 1),), dec_batch=batch, seed=200 + case)
+        wl = W.make_workload(cfg, dec_lens=lens)
+        dw = DeviceWorkload(wl)
+        part = None
+        try:
+            if decode_cus < 256:
+                part = Partition(256 - decode_cus, decode_cus)
+                stream = part.decode_stream
+            else:
+                stream = 0
+            got = to_bits(dw.decode(stream))
+            torch.cuda.synchronize()
+        finally:
+            if part is not None:
+                part.close()
+            dw.close()
+        ref = oracle.decode(wl.q_dec, wl.k_pool, wl.v_pool, wl.dec_bt, wl.dec_lens)
+        assert_close(got, ref, f"decode random case {case}")
