@@ -41,13 +41,20 @@ void planners() {
         mw_kv_pool *pool = nullptr;
         check(mw_kv_pool_create(&desc, g_fake, g_fake, &pool) == MW_OK, "pool create", it);
         const mw_attn_shape shape{hkv * group, hkv, 128, 0.0883883f};
-        // decode: lengths on page edges, long and short, occasionally invalid
-        const int batch = uniform(0, 300);
+        // decode: lengths on page edges, long and short, occasionally invalid;
+        // a quarter of the batches are a few long sequences (equal or not),
+        // whose segments the balanced split may pad to whole ranges
+        const bool few_long = uniform(0, 3) == 0;
+        const int batch = few_long ? uniform(1, 6) : uniform(0, 300);
+        const bool equal = few_long && uniform(0, 1) == 0;
         std::vector<int32_t> lens(batch);
         int max_len = 1;
         for (int b = 0; b < batch; ++b) {
             const int kind = uniform(0, 9);
-            lens[b] = kind == 0 ? 16 * uniform(1, 64) : kind == 1 ? uniform(1, 17) : uniform(1, 70000);
+            if (few_long)
+                lens[b] = equal && b > 0 ? lens[0] : uniform(2000, 70000);
+            else
+                lens[b] = kind == 0 ? 16 * uniform(1, 64) : kind == 1 ? uniform(1, 17) : uniform(1, 70000);
             max_len = lens[b] > max_len ? lens[b] : max_len;
         }
         if (batch > 0 && uniform(0, 49) == 0) lens[uniform(0, batch - 1)] = uniform(-3, 0);
@@ -67,6 +74,14 @@ void planners() {
             // per-sequence chunk bases, or the balanced split's per-slot done flags
             const size_t meta = dp.per_unit > 0 ? static_cast<size_t>(dp.slots) * 4 : static_cast<size_t>(batch) * 4;
             check(dp.off_meta + meta <= dp.bytes, "workspace holds the flags", it);
+            if (dp.aligned) {  // segments padded to whole ranges: one piece of one segment per unit
+                int64_t padded = 0;
+                for (int b = 0; b < batch; ++b)
+                    padded += (static_cast<int64_t>(lens[b] + 15) / 16 + dp.per_unit - 1) / dp.per_unit * dp.per_unit;
+                check(dp.per_unit >= 16 && dp.total == padded * hkv && dp.units * dp.per_unit == dp.total,
+                      "aligned split covers every padded segment in whole ranges", it);
+                check(cus > 0 && dp.units <= std::min<int64_t>(2 * cus, 512), "aligned split within the units", it);
+            }
         }
         if (st != MW_OK) check(st2 != MW_OK, "a refused size is refused by the plan too", it);
         // prefill: varlen batches, prefixes, tables that are too short
