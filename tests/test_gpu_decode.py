@@ -271,3 +271,40 @@ def test_decode_random_batches_on_partitions():
             dw.close()
         ref = oracle.decode(wl.q_dec, wl.k_pool, wl.v_pool, wl.dec_bt, wl.dec_lens)
         assert_close(got, ref, f"decode random case {case}")
+
+
+def test_decode_graph_replays_reuse_the_tag():
+    """A decode call captured in a graph replays with the tag it was captured
+    with: the merging work-group clears the segment's flags, so every replay
+    merges again, also with eager calls (other tags) on the same workspace
+    in between.  One 20,001-token sequence on the whole GPU: a split whose
+    segments are padded to whole ranges."""
+    say("decode graph replays")
+    cfg = W.custom_config(hq=32, hkv=8, pre_chunks=((0, 1),), dec_batch=1, seed=91)
+    wl = W.make_workload(cfg, dec_lens=[20001])
+    dw = DeviceWorkload(wl)
+    try:
+        ref = to_bits(dw.decode()).copy()
+        torch.cuda.synchronize()
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            dw.decode(s.cuda_stream)  # warm-up on the capture stream
+        s.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            dw.decode(torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        other = torch.empty_like(dw.o_dec)
+        for rep in range(4):
+            dw.o_dec.zero_()
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            assert np.array_equal(to_bits(dw.o_dec), ref), f"replay {rep}"
+            dw.decode(out=other)  # an eager call with its own tag, same workspace
+            torch.cuda.synchronize()
+            assert np.array_equal(to_bits(other), ref), f"eager call after replay {rep}"
+        del g
+    finally:
+        dw.close()
+    assert_close(ref, oracle.decode(wl.q_dec, wl.k_pool, wl.v_pool, wl.dec_bt, wl.dec_lens), "decode graph case")
