@@ -83,22 +83,28 @@ def test_prefill_page_permutation_invariance_and_determinism():
     assert np.array_equal(a, run_prefill(wl2, 40, 150)), "page renumbering changed the result"
 
 
+def _varlen_setup(seqs, hq, hkv, seed0):
+    """One pool holding every sequence's pages (the workloads' pools laid end
+    to end, tables offset), their block-table rows, and the batch's Q rows."""
+    cfgs = [W.custom_config(hq=hq, hkv=hkv, pre_chunks=((r, n),), dec_batch=1, dec_len_lo=1,
+                            dec_len_hi=2, seed=seed0 + i) for i, (r, n) in enumerate(seqs)]
+    wls = [W.make_workload(c) for c in cfgs]
+    k = np.concatenate([w.k_pool for w in wls]); v = np.concatenate([w.v_pool for w in wls])
+    offs = np.cumsum([0] + [w.num_pages for w in wls])
+    stride = max(len(w.pre_bt) for w in wls)
+    bt = np.full((len(seqs), stride), 0, np.int32)
+    for i, w in enumerate(wls):
+        bt[i, :len(w.pre_bt)] = w.pre_bt + offs[i]
+    q = np.concatenate([w.q_pre[r:r + n] for w, (r, n) in zip(wls, seqs)])
+    return wls, k, v, bt, stride, q
+
+
 def test_prefill_varlen_batch():
     """Three sequences in one call (block-table rows, varlen Q/O offsets)."""
     say("prefill varlen batch")
     from paper_2504_14489_amd import mw
     seqs = [(0, 70), (20, 5), (130, 64)]
-    cfgs = [W.custom_config(hq=8, hkv=2, pre_chunks=((r, n),), dec_batch=1, dec_len_lo=1,
-                            dec_len_hi=2, seed=40 + i) for i, (r, n) in enumerate(seqs)]
-    wls = [W.make_workload(c) for c in cfgs]
-    # one pool holding all three sequences: concatenate pools and offset their tables
-    k = np.concatenate([w.k_pool for w in wls]); v = np.concatenate([w.v_pool for w in wls])
-    offs = np.cumsum([0] + [w.num_pages for w in wls])
-    stride = max(len(w.pre_bt) for w in wls)
-    bt = np.full((3, stride), 0, np.int32)
-    for i, w in enumerate(wls):
-        bt[i, :len(w.pre_bt)] = w.pre_bt + offs[i]
-    q = np.concatenate([w.q_pre[r:r + n] for w, (r, n) in zip(wls, seqs)])
+    wls, k, v, bt, stride, q = _varlen_setup(seqs, 8, 2, 40)
     dev = torch.device("cuda:0")
     t16 = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev)
     t32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
@@ -120,6 +126,65 @@ def test_prefill_varlen_batch():
         ref = oracle.prefill(w.q_pre[r:r + n], w.k_pool, w.v_pool, w.pre_bt, r)
         assert_close(got[row:row + n], ref, f"varlen seq r={r} n={n}")
         row += n
+
+
+def test_prefill_varlen_batch_with_the_split_on_partitions():
+    """Four sequences of different prefixes and lengths in one call, through
+    the split-enabled entry point on 8 and 96 CUs and the whole GPU (the plan
+    cuts the long-prefix sequence's blocks into key ranges), and through the
+    plain one: every row against the oracle, and the plain and split calls
+    within the tolerance of each other."""
+    from paper_2504_14489_amd import mw
+    from paper_2504_14489_amd.device import Partition
+    hq, hkv = 8, 2
+    seqs = [(0, 700), (5000, 90), (300, 1500), (12000, 33)]
+    say(f"prefill varlen batch with the split: {seqs}")
+    wls, k, v, bt, stride, q = _varlen_setup(seqs, hq, hkv, 60)
+    dev = torch.device("cuda:0")
+    t16 = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev)
+    t32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
+    dk, dv, dq, dbt = t16(k), t16(v), t16(q), t32(bt)
+    ns, rs = [n for _, n in seqs], [r for r, _ in seqs]
+    indptr, pref = t32(np.cumsum([0] + ns)), t32(rs)
+    pool = mw.mw_kv_pool_create(k.shape[0], 16, hkv, 128, dk.data_ptr(), dv.data_ptr())
+    results, cut = {}, {}
+    try:
+        for cus in (8, 96, 0):
+            part = Partition(cus, 256 - cus) if cus else None
+            stream = part.prefill_stream if part else 0
+            try:
+                nbytes = mw.mw_prefill_workspace_size(hq, hkv, 128, ns, rs, cus or 256)
+                ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=dev)
+                for split in (True, False):
+                    do = torch.zeros_like(dq)
+                    t = Timing()
+                    if split:
+                        mw.mw_prefill_attn_ws(pool, hq, hkv, 128, 1 / np.sqrt(128), ns, rs, indptr.data_ptr(),
+                                              pref.data_ptr(), dbt.data_ptr(), stride, dq.data_ptr(), do.data_ptr(),
+                                              ws.data_ptr(), ws.numel(), stream, t.h)
+                    else:
+                        mw.mw_prefill_attn(pool, hq, hkv, 128, 1 / np.sqrt(128), ns, rs, indptr.data_ptr(),
+                                           pref.data_ptr(), dbt.data_ptr(), stride, dq.data_ptr(), do.data_ptr(),
+                                           stream, t.h)
+                    torch.cuda.synchronize()
+                    results[(cus, split)] = to_bits(do).copy()
+                    if split:
+                        cut[cus] = (mw.mw_timing_kernels(t.h) == 2, nbytes > 0)
+                    t.close()
+            finally:
+                if part:
+                    part.close()
+    finally:
+        mw.mw_kv_pool_destroy(pool)
+    for cus, (two_kernels, planned) in cut.items():
+        assert two_kernels == planned, f"{cus} CUs: the call and the workspace size disagree on the cut"
+    assert any(planned for _, planned in cut.values()), "no partition cut the batch"
+    refs = [oracle.prefill(w.q_pre[r:r + n], w.k_pool, w.v_pool, w.pre_bt, r) for w, (r, n) in zip(wls, seqs)]
+    for (cus, split), got in results.items():
+        row = 0
+        for ref, (r, n) in zip(refs, seqs):
+            assert_close(got[row:row + n], ref, f"varlen r={r} n={n} on {cus or 'all'} CUs, split={split}")
+            row += n
 
 
 def test_prefill_same_result_on_any_cu_count():
