@@ -25,15 +25,19 @@ def noalloc_decode(dw, stream=0, chunk_pages=0):
 @pytest.mark.parametrize("chunk_pages", [0, -1])
 def test_noalloc_decode_equals_the_workspace_call_twice_in_a_row(chunk_pages):
     """Two calls in a row, the second on a smaller batch (the array keeps the
-    first call's partials), each bit-equal to mw_decode_attn with a caller
-    workspace on the same stream, and within tolerance of the oracle."""
+    first call's partials), then two long sequences (whose segments the
+    balanced split pads to whole ranges), each bit-equal to mw_decode_attn
+    with a caller workspace on the same stream, and within tolerance of the
+    oracle."""
     part = Partition(64, 192)
     try:
-        for name, cfg in (("llama8b", W.CONFIGS["llama8b"]),
-                          ("small", W.custom_config(hq=32, hkv=8, pre_chunks=((0, 1),), dec_batch=9,
-                                                    dec_len_lo=1, dec_len_hi=700, seed=12))):
+        for name, cfg, lens in (("llama8b", W.CONFIGS["llama8b"], None),
+                                ("small", W.custom_config(hq=32, hkv=8, pre_chunks=((0, 1),), dec_batch=9,
+                                                          dec_len_lo=1, dec_len_hi=700, seed=12), None),
+                                ("two_long", W.custom_config(hq=32, hkv=8, pre_chunks=((0, 1),), dec_batch=2,
+                                                             seed=13), [20000, 15000])):
             say(f"noalloc decode {name} chunk_pages={chunk_pages}")
-            wl = W.make_workload(cfg)
+            wl = W.make_workload(cfg, dec_lens=lens) if lens else W.make_workload(cfg)
             dw = DeviceWorkload(wl)
             try:
                 got = to_bits(noalloc_decode(dw, part.decode_stream, chunk_pages))
